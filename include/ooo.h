@@ -1,0 +1,203 @@
+/*
+ * ooo.h - C ABI of libooo, the MI355X (gfx950) tree-verification library.
+ *
+ * One verification step of greedy speculative decoding at batch one, as the
+ * OoO-Spec paper describes it (Section 3, "Target authority" with Eq. 1 and
+ * "The ToolSpec decoding loop"; Section 4.4, "Verify and commit"):
+ *
+ *   ooo_pack_tree      merge priority-ordered draft continuations into a trie
+ *   ooo_tree_attn      per layer: every trie node attends to the committed
+ *                      prefix and to its own ancestors (one pass for the tree)
+ *   ooo_lmhead_argmax  LM head over all nodes and the greedy token of each
+ *   ooo_accept         longest root path whose tokens agree with the greedy
+ *                      tokens, plus the target's own next (bonus) token
+ *   ooo_kv_compact     move the accepted nodes' K/V rows into the committed
+ *                      cache, directly after the prefix
+ *
+ * Conventions shared by every entry point
+ *   - Return value: OOO_OK (0) or a negative ooo_status.  On error nothing has
+ *     been enqueued and ooo_last_error() returns a message (thread-local,
+ *     valid until the next call on the same thread).
+ *   - Arguments are validated on the host before any device work is queued.
+ *   - Device entry points are asynchronous on `stream` (a hipStream_t; NULL is
+ *     the null stream) and return after enqueueing.  Buffers must stay valid
+ *     until that work completes.  They never allocate device memory; scratch
+ *     comes from the caller's `workspace`, sized by the *_workspace query.
+ *   - The caller owns every buffer.  Outputs must not alias inputs unless an
+ *     entry point says so.  No entry point keeps state between calls.
+ *   - Calls sharing a workspace must not run concurrently.
+ *   - dtype: OOO_F32 (float32 everywhere) or OOO_BF16 (bfloat16 storage,
+ *     float32 accumulation and softmax).
+ *   - Results are deterministic: identical inputs give bitwise-identical
+ *     outputs (no floating-point atomics).
+ */
+#ifndef OOO_H
+#define OOO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define OOO_ABI_VERSION 1
+
+typedef enum {
+  OOO_OK = 0,
+  OOO_ERR_INVALID = -1,     /* null pointer, bad size, inconsistent shape */
+  OOO_ERR_UNSUPPORTED = -2, /* valid request this build has no kernel for */
+  OOO_ERR_CAPACITY = -3,    /* an output or workspace is too small */
+  OOO_ERR_HIP = -4          /* the HIP runtime reported a launch error */
+} ooo_status;
+
+typedef enum { OOO_F32 = 0, OOO_BF16 = 1 } ooo_dtype;
+
+/* Message for the last non-OK status on this thread ("" if none). */
+const char* ooo_last_error(void);
+
+/* OOO_ABI_VERSION of the loaded library. */
+int ooo_version(void);
+
+/*
+ * ooo_pack_tree - candidate trie (Section 3, ToolSpec loop: candidates are
+ * combined into one tree; Section 4.3: Merge_B keeps a fixed candidate
+ * budget and hint lanes come first; Section 4.4: hint and native
+ * continuations are compiled into the same tree).
+ *
+ * HOST memory only, synchronous.
+ *   root_token      the token the target committed last (node 0)
+ *   cand_tokens     concatenated candidate continuations (after the root)
+ *   cand_offsets    [n_cand + 1] CSR offsets into cand_tokens, in priority
+ *                   order, non-decreasing, cand_offsets[0] == 0
+ *   max_nodes       node budget (>= 1), including the root
+ *   max_depth       depth cap (>= 0); the root has depth 0
+ *   token, parent, depth   [max_nodes] int32 outputs; parent[0] == -1
+ *   anc_mask        [max_nodes * mask_words] uint64 output; bit j of row i is
+ *                   set iff node j is an ancestor of node i or i itself
+ *   mask_words      words per mask row; must satisfy 64 * mask_words >= max_nodes
+ *   n_nodes         number of nodes written
+ *   n_truncated     candidate tokens dropped by the depth cap or the budget
+ * Nodes appear in first-appearance order over the candidates, so
+ * parent[i] < i and siblings carry distinct tokens.  A token equal to an
+ * existing child is shared; once the budget is full no node is added and the
+ * rest of each candidate from its first unplaceable token is dropped.
+ * Errors: OOO_ERR_INVALID for null pointers, n_cand < 0, max_nodes < 1,
+ * max_depth < 0, non-monotone offsets, negative tokens, or too few mask words.
+ */
+int ooo_pack_tree(int32_t root_token, const int32_t* cand_tokens, const int32_t* cand_offsets,
+                  int32_t n_cand, int32_t max_nodes, int32_t max_depth, int32_t* token,
+                  int32_t* parent, int32_t* depth, uint64_t* anc_mask, int32_t mask_words,
+                  int32_t* n_nodes, int32_t* n_truncated);
+
+/*
+ * ooo_tree_attn - one layer of tree-masked attention (Section 4.4: the target
+ * scores the whole candidate tree in one forward pass; each node sees what
+ * sequential greedy decoding of its own path would see).
+ *
+ * DEVICE pointers.
+ *   q          [n_nodes][n_q_heads][head_dim] queries (post-RoPE)
+ *   k_cache, v_cache   one layer, [n_kv_heads][cap][head_dim]: rows [0, P) are
+ *              the committed prefix, row P + i holds node i's key/value
+ *   cap        rows per KV head; P + n_nodes <= cap
+ *   prefix_len P >= 0
+ *   anc_mask   [n_nodes][mask_words] from ooo_pack_tree (device copy)
+ *   scale      score scale, normally 1/sqrt(head_dim)
+ *   out        [n_nodes][n_q_heads][head_dim], same dtype; must not alias
+ * Query head h reads KV head h / (n_q_heads / n_kv_heads).  For node i the
+ * keys are prefix rows 0..P-1 and rows P + j for every j set in anc_mask[i];
+ * softmax in float32.
+ * Supported: head_dim 64 or 128; n_q_heads / n_kv_heads <= 8 for OOO_BF16;
+ * n_nodes <= 64 * mask_words <= 1024.
+ * Errors: OOO_ERR_INVALID (null pointers, n_nodes < 1, prefix_len < 0,
+ * P + n_nodes > cap, n_q_heads % n_kv_heads != 0, 64 * mask_words < n_nodes),
+ * OOO_ERR_UNSUPPORTED, OOO_ERR_CAPACITY (ws_bytes below the query),
+ * OOO_ERR_HIP.
+ */
+size_t ooo_tree_attn_workspace(int32_t n_nodes, int32_t n_q_heads, int32_t n_kv_heads,
+                               int32_t head_dim, int32_t prefix_len, ooo_dtype dt);
+int ooo_tree_attn(const void* q, const void* k_cache, const void* v_cache, int64_t cap,
+                  int32_t prefix_len, int32_t n_nodes, const uint64_t* anc_mask,
+                  int32_t mask_words, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                  float scale, ooo_dtype dt, void* out, void* workspace, size_t ws_bytes,
+                  void* stream);
+
+/*
+ * ooo_lmhead_argmax - LM head and greedy token of every node (Eq. 1: the
+ * committed token is the target's most likely next token).
+ *
+ * DEVICE pointers.
+ *   hidden     [n_nodes][hidden_dim] final hidden rows
+ *   weight     [vocab][hidden_dim] (nn.Linear layout)
+ *   argmax_ids [n_nodes] int32: lowest vocabulary index among equal maxima
+ *   max_logit  [n_nodes] float32: the logit at argmax_ids
+ *   logits     NULL, or [n_nodes][vocab] float32 (validation dump)
+ * Logits are float32 sums of exact products.
+ * Supported: OOO_BF16 needs hidden_dim % 64 == 0 and n_nodes <= 256;
+ * OOO_F32 needs hidden_dim % 4 == 0.
+ * Errors: OOO_ERR_INVALID (null pointers, non-positive sizes),
+ * OOO_ERR_UNSUPPORTED, OOO_ERR_CAPACITY, OOO_ERR_HIP.
+ */
+size_t ooo_lmhead_workspace(int32_t n_nodes, int32_t hidden_dim, int32_t vocab, ooo_dtype dt);
+int ooo_lmhead_argmax(const void* hidden, const void* weight, int32_t n_nodes,
+                      int32_t hidden_dim, int32_t vocab, ooo_dtype dt, int32_t* argmax_ids,
+                      float* max_logit, float* logits, void* workspace, size_t ws_bytes,
+                      void* stream);
+
+/*
+ * ooo_accept - longest greedy-agreeing root path (Section 4.4, Verify and
+ * commit: draft tokens are kept while they equal the target's greedy token
+ * at their parent; at the first disagreement the rest is rejected and the
+ * target's own token is used).
+ *
+ * DEVICE pointers.
+ *   token, parent, depth, anc_mask   the packed trie (ooo_pack_tree layout)
+ *   argmax_ids   [n_nodes] greedy token of every node
+ *   path_cap     entries in `path`; must exceed the trie's deepest depth
+ *   path         [path_cap] int32 out: path[d] = accepted node at depth d for
+ *                d <= L, -1 beyond; path[0] == 0
+ *   accept_len   [1] int32 out: L, the number of accepted draft nodes
+ *   bonus_token  [1] int32 out: argmax_ids[path[L]]
+ * The step commits token[path[1..L]] followed by the bonus token (L + 1
+ * tokens).  Precondition (guaranteed by ooo_pack_tree): parent[i] < i and
+ * siblings carry distinct tokens.
+ * Errors: OOO_ERR_INVALID (null pointers, n_nodes < 1, path_cap < 1,
+ * 64 * mask_words < n_nodes, mask_words > 16), OOO_ERR_HIP.
+ */
+int ooo_accept(const int32_t* token, const int32_t* parent, const int32_t* depth,
+               const uint64_t* anc_mask, int32_t mask_words, const int32_t* argmax_ids,
+               int32_t n_nodes, int32_t path_cap, int32_t* path, int32_t* accept_len,
+               int32_t* bonus_token, void* stream);
+
+/*
+ * ooo_kv_compact - commit the accepted states (Section 4.4: only states on
+ * the accepted path enter the committed KV cache).
+ *
+ * DEVICE pointers.
+ *   k_cache, v_cache   [n_layers][n_kv_heads][cap][head_dim], updated in place
+ *   prefix_len         P, the committed length before this step
+ *   n_nodes            trie size of the step; node rows are [P, P + n_nodes)
+ *   path, accept_len   outputs of ooo_accept (read on the device, so no host
+ *                      synchronisation is needed in between)
+ *   path_cap           entries in `path`
+ * For every layer, KV head, K and V: row P + path[d] moves to row P + d for
+ * d = 0..L.  The committed length becomes P + L + 1; rows beyond it are free.
+ * Rows [0, P] are never written.  Overlapping source and destination rows are
+ * handled (every source is read before its row can be overwritten).
+ * Precondition: path is strictly increasing (true for any root path of a
+ * packed trie).  Entries with path[d] >= n_nodes or L >= path_cap are
+ * ignored on the device rather than read out of bounds.
+ * Errors: OOO_ERR_INVALID (null pointers, sizes < 1, prefix_len < 0,
+ * prefix_len + n_nodes > cap), OOO_ERR_UNSUPPORTED (head_dim * element size
+ * not a multiple of 16 bytes), OOO_ERR_HIP.
+ */
+int ooo_kv_compact(void* k_cache, void* v_cache, int32_t n_layers, int32_t n_kv_heads,
+                   int64_t cap, int32_t head_dim, ooo_dtype dt, int32_t prefix_len,
+                   int32_t n_nodes, const int32_t* path, const int32_t* accept_len,
+                   int32_t path_cap, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OOO_H */

@@ -1,0 +1,158 @@
+// Greedy acceptance and cache compaction (Section 4.4, Verify and commit:
+// draft tokens are kept while they match the target's greedy token at their
+// parent, the first mismatch ends the run and the target's own token follows;
+// only the accepted states are committed to the KV cache).
+//
+// ooo_accept runs in one block.  Node i "matches" when it is the root or its
+// token equals the greedy token of its parent; the match bits of 64 nodes are
+// one wavefront ballot, so they land directly in the layout of the ancestor
+// bitmask.  A node is accepted iff every ancestor-or-self matches, i.e.
+// (anc_mask[i] & ~match) == 0.  Because siblings carry distinct tokens the
+// accepted nodes form one root path; its length is a max-reduction over their
+// depths and path[depth[i]] = i places each of them.
+//
+// ooo_kv_compact moves row P + path[d] to row P + d for every layer, KV head,
+// K and V.  One block per (layer, head, K|V) slice; each pass reads up to 64
+// source rows into registers, synchronises, then writes them.  This is safe
+// in place: path is strictly increasing with path[d] >= d, so a pass only
+// overwrites rows below every source row of the later passes.
+#include "device_common.h"
+#include "ooo_internal.h"
+
+namespace ooo {
+namespace {
+
+constexpr int kMaxMaskWords = 16;
+
+__global__ __launch_bounds__(1024) void accept_kernel(const int32_t* __restrict__ token,
+                                                      const int32_t* __restrict__ parent,
+                                                      const int32_t* __restrict__ depth,
+                                                      const uint64_t* __restrict__ anc, int W,
+                                                      const int32_t* __restrict__ ids, int N, int path_cap,
+                                                      int32_t* __restrict__ path, int32_t* __restrict__ accept_len,
+                                                      int32_t* __restrict__ bonus) {
+  __shared__ uint64_t match[kMaxMaskWords];
+  __shared__ int best_depth;
+  const int tid = threadIdx.x;
+  if (tid == 0) best_depth = 0;
+  for (int i = tid; i < path_cap; i += blockDim.x) path[i] = -1;
+  for (int w = tid; w < W; w += blockDim.x) match[w] = 0;
+  __syncthreads();
+  // match bits, one ballot per 64 nodes
+  for (int base = 0; base < 64 * W; base += blockDim.x) {
+    const int i = base + tid;
+    bool m = false;
+    if (i < N) m = (i == 0) || (token[i] == ids[parent[i]]);
+    const uint64_t bits = __ballot(m);
+    if ((tid & 63) == 0 && i < 64 * W) match[i >> 6] = bits;
+  }
+  __syncthreads();
+  for (int i = tid; i < N; i += blockDim.x) {
+    bool ok = true;
+    for (int w = 0; w < W; ++w) ok = ok && ((anc[(size_t)i * W + w] & ~match[w]) == 0);
+    if (ok) {
+      const int d = depth[i];
+      if (d < path_cap) {
+        path[d] = i;
+        atomicMax(&best_depth, d);
+      }
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    const int L = best_depth;
+    *accept_len = L;
+    *bonus = ids[path[L]];
+  }
+}
+
+__global__ __launch_bounds__(256) void kv_compact_kernel(uint8_t* __restrict__ k, uint8_t* __restrict__ v,
+                                                         int Hkv, long long cap, int row_bytes, int P, int N,
+                                                         const int32_t* __restrict__ path,
+                                                         const int32_t* __restrict__ accept_len, int path_cap) {
+  const int slice = blockIdx.x;  // (layer * Hkv + head) * 2 + (K or V)
+  uint8_t* base = ((slice & 1) ? v : k) + (size_t)(slice >> 1) * cap * row_bytes;
+  int L = *accept_len;
+  if (L > path_cap - 1) L = path_cap - 1;
+  const int chunks = row_bytes / 16;  // 16-byte pieces per row
+  constexpr int R = 4;                // pieces per thread per pass
+  const int rows_per_pass = (256 * R) / chunks;
+  for (int d0 = 1; d0 <= L; d0 += rows_per_pass) {
+    u32x4 buf[R];
+    int dst[R];
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+      const int item = threadIdx.x + 256 * i;
+      const int d = d0 + item / chunks, ch = item % chunks;
+      dst[i] = -1;
+      if (item < rows_per_pass * chunks && d <= L && d < N) {
+        const int src = path[d];
+        if (src >= 0 && src < N) {
+          buf[i] = ld16(base + (size_t)(P + src) * row_bytes + 16 * ch);
+          dst[i] = d;
+        }
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+      const int item = threadIdx.x + 256 * i;
+      if (dst[i] >= 0) st16(base + (size_t)(P + dst[i]) * row_bytes + 16 * (item % chunks), buf[i]);
+    }
+    __syncthreads();
+  }
+}
+
+}  // namespace
+}  // namespace ooo
+
+using namespace ooo;
+
+extern "C" int ooo_accept(const int32_t* token, const int32_t* parent, const int32_t* depth,
+                          const uint64_t* anc_mask, int32_t mask_words, const int32_t* argmax_ids,
+                          int32_t n_nodes, int32_t path_cap, int32_t* path, int32_t* accept_len,
+                          int32_t* bonus_token, void* stream) {
+  OOO_REQUIRE(token && parent && depth && anc_mask && argmax_ids && path && accept_len && bonus_token,
+              OOO_ERR_INVALID, "ooo_accept: null pointer");
+  OOO_REQUIRE(n_nodes >= 1, OOO_ERR_INVALID, "ooo_accept: n_nodes must be >= 1");
+  OOO_REQUIRE(path_cap >= 1, OOO_ERR_INVALID, "ooo_accept: path_cap must be >= 1");
+  OOO_REQUIRE(mask_words >= 1 && mask_words <= kMaxMaskWords && (int64_t)mask_words * 64 >= n_nodes,
+              OOO_ERR_INVALID, "ooo_accept: mask_words=%d cannot describe %d nodes (max %d words)", mask_words,
+              n_nodes, kMaxMaskWords);
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  int threads = 64 * mask_words;
+  if (threads > 1024) threads = 1024;
+  accept_kernel<<<1, threads, 0, st>>>(token, parent, depth, anc_mask, mask_words, argmax_ids, n_nodes, path_cap,
+                                       path, accept_len, bonus_token);
+  const hipError_t e = hipGetLastError();
+  OOO_REQUIRE(e == hipSuccess, OOO_ERR_HIP, "ooo_accept: launch failed: %s", hipGetErrorString(e));
+  return ooo::ok();
+}
+
+extern "C" int ooo_kv_compact(void* k_cache, void* v_cache, int32_t n_layers, int32_t n_kv_heads, int64_t cap,
+                              int32_t head_dim, ooo_dtype dt, int32_t prefix_len, int32_t n_nodes,
+                              const int32_t* path, const int32_t* accept_len, int32_t path_cap, void* stream) {
+  OOO_REQUIRE(k_cache && v_cache && path && accept_len, OOO_ERR_INVALID, "ooo_kv_compact: null pointer");
+  OOO_REQUIRE(n_layers >= 1 && n_kv_heads >= 1 && head_dim >= 1 && n_nodes >= 1 && path_cap >= 1,
+              OOO_ERR_INVALID, "ooo_kv_compact: sizes must be positive");
+  OOO_REQUIRE(prefix_len >= 0 && (int64_t)prefix_len + n_nodes <= cap, OOO_ERR_INVALID,
+              "ooo_kv_compact: prefix_len + n_nodes (%lld) exceeds cap (%lld)", (long long)prefix_len + n_nodes,
+              (long long)cap);
+  OOO_REQUIRE(dt == OOO_F32 || dt == OOO_BF16, OOO_ERR_INVALID, "ooo_kv_compact: unknown dtype %d", (int)dt);
+  const int esz = dt == OOO_F32 ? 4 : 2;
+  const int row_bytes = head_dim * esz;
+  OOO_REQUIRE(row_bytes % 16 == 0 && row_bytes <= 1024 * 16, OOO_ERR_UNSUPPORTED,
+              "ooo_kv_compact: row of %d bytes is not a multiple of 16 (or too long)", row_bytes);
+  OOO_REQUIRE((int64_t)n_layers * n_kv_heads * 2 <= 0x7FFFFFFF, OOO_ERR_UNSUPPORTED, "ooo_kv_compact: too many slices");
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const dim3 grid(n_layers * n_kv_heads * 2);
+  if (esz == 2)
+    kv_compact_kernel<<<grid, 256, 0, st>>>((uint8_t*)k_cache, (uint8_t*)v_cache, n_kv_heads, cap, row_bytes,
+                                                prefix_len, n_nodes, path, accept_len, path_cap);
+  else
+    kv_compact_kernel<<<grid, 256, 0, st>>>((uint8_t*)k_cache, (uint8_t*)v_cache, n_kv_heads, cap, row_bytes,
+                                                prefix_len, n_nodes, path, accept_len, path_cap);
+  const hipError_t e = hipGetLastError();
+  OOO_REQUIRE(e == hipSuccess, OOO_ERR_HIP, "ooo_kv_compact: launch failed: %s", hipGetErrorString(e));
+  return ooo::ok();
+}

@@ -1,0 +1,204 @@
+"""ctypes binding of libooo (C ABI declared in include/ooo.h).
+
+Argument marshalling only: every computation happens in the native library.
+Device arguments are torch tensors on the ROCm device (their ``data_ptr()``
+is passed through); host arguments of ``pack_tree`` are NumPy arrays.  The
+library must be built (``python -m paper_2608_00814_amd.build``); loading
+fails loudly when it is missing.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libooo.so")
+
+OK, ERR_INVALID, ERR_UNSUPPORTED, ERR_CAPACITY, ERR_HIP = 0, -1, -2, -3, -4
+F32, BF16 = 0, 1
+
+_c_i32p = ctypes.POINTER(ctypes.c_int32)
+_c_u64p = ctypes.POINTER(ctypes.c_uint64)
+_vp = ctypes.c_void_p
+_i32 = ctypes.c_int32
+_i64 = ctypes.c_int64
+_sz = ctypes.c_size_t
+
+# name -> (restype, argtypes); mirrors include/ooo.h
+SIGNATURES = {
+    "ooo_last_error": (ctypes.c_char_p, []),
+    "ooo_version": (ctypes.c_int, []),
+    "ooo_pack_tree": (ctypes.c_int, [_i32, _c_i32p, _c_i32p, _i32, _i32, _i32, _c_i32p, _c_i32p, _c_i32p,
+                                     _c_u64p, _i32, _c_i32p, _c_i32p]),
+    "ooo_tree_attn_workspace": (_sz, [_i32, _i32, _i32, _i32, _i32, ctypes.c_int]),
+    "ooo_tree_attn": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _i32, _vp, _i32, _i32, _i32, _i32,
+                                     ctypes.c_float, ctypes.c_int, _vp, _vp, _sz, _vp]),
+    "ooo_lmhead_workspace": (_sz, [_i32, _i32, _i32, ctypes.c_int]),
+    "ooo_lmhead_argmax": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, ctypes.c_int, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "ooo_accept": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i32, _vp, _i32, _i32, _vp, _vp, _vp, _vp]),
+    "ooo_kv_compact": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i64, _i32, ctypes.c_int, _i32, _i32, _vp, _vp,
+                                      _i32, _vp]),
+}
+
+
+class OooError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"[{status}] {message}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise OSError(f"{LIB_PATH} is missing: build it with `python -m paper_2608_00814_amd.build`")
+        h = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            f = getattr(h, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = h
+    return _lib
+
+
+def last_error() -> str:
+    return lib().ooo_last_error().decode()
+
+
+def version() -> int:
+    return int(lib().ooo_version())
+
+
+def _check(status: int) -> None:
+    if status != OK:
+        raise OooError(status, last_error())
+
+
+def dtype_code(t) -> int:
+    import torch
+
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _dev(t, name: str, contiguous: bool = True):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if contiguous and not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+
+        return torch.cuda.current_stream().cuda_stream
+    return int(stream) if not hasattr(stream, "cuda_stream") else stream.cuda_stream
+
+
+# ----------------------------------------------------------------------------
+# host
+
+
+def pack_tree(root_token: int, cand_tokens: np.ndarray, cand_offsets: np.ndarray, max_nodes: int, max_depth: int,
+              mask_words: Optional[int] = None) -> dict:
+    """ooo_pack_tree on NumPy arrays; outputs trimmed to n_nodes."""
+    W = mask_words if mask_words is not None else max(1, (max_nodes + 63) // 64)
+    toks = np.ascontiguousarray(cand_tokens, dtype=np.int32)
+    offs = np.ascontiguousarray(cand_offsets, dtype=np.int32)
+    cap = max(int(max_nodes), 1)
+    token = np.zeros(cap, np.int32)
+    parent = np.zeros(cap, np.int32)
+    depth = np.zeros(cap, np.int32)
+    mask = np.zeros(cap * W, np.uint64)
+    n = ctypes.c_int32(0)
+    trunc = ctypes.c_int32(0)
+    st = lib().ooo_pack_tree(int(root_token), toks.ctypes.data_as(_c_i32p) if toks.size else None,
+                             offs.ctypes.data_as(_c_i32p), len(offs) - 1, int(max_nodes), int(max_depth),
+                             token.ctypes.data_as(_c_i32p), parent.ctypes.data_as(_c_i32p),
+                             depth.ctypes.data_as(_c_i32p), mask.ctypes.data_as(_c_u64p), int(W),
+                             ctypes.byref(n), ctypes.byref(trunc))
+    _check(st)
+    k = n.value
+    return {"token": token[:k].copy(), "parent": parent[:k].copy(), "depth": depth[:k].copy(),
+            "anc_mask": mask.reshape(cap, W)[:k].copy(), "n_nodes": k, "n_truncated": trunc.value,
+            "mask_words": W}
+
+
+# ----------------------------------------------------------------------------
+# device
+
+
+def tree_attn_workspace(n_nodes: int, n_q_heads: int, n_kv_heads: int, head_dim: int, prefix_len: int,
+                        dtype: int) -> int:
+    return int(lib().ooo_tree_attn_workspace(n_nodes, n_q_heads, n_kv_heads, head_dim, prefix_len, dtype))
+
+
+def tree_attn(q, k_cache, v_cache, prefix_len: int, n_nodes: int, anc_mask, n_q_heads: int, n_kv_heads: int,
+              scale: float, out, workspace=None, stream=None) -> None:
+    """q [N][Hq][D]; k_cache/v_cache one layer [Hkv][cap][D]; anc_mask
+    [N][W] int64/uint64 device tensor; out [N][Hq][D]."""
+    for t, nm in ((q, "q"), (k_cache, "k_cache"), (v_cache, "v_cache"), (anc_mask, "anc_mask"), (out, "out")):
+        _dev(t, nm)
+    Hkv, cap, D = k_cache.shape
+    W = anc_mask.shape[-1]
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().ooo_tree_attn(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), cap, prefix_len, n_nodes,
+                               anc_mask.data_ptr(), W, n_q_heads, n_kv_heads, D, float(scale), dtype_code(q),
+                               out.data_ptr(), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def lmhead_workspace(n_nodes: int, hidden_dim: int, vocab: int, dtype: int) -> int:
+    return int(lib().ooo_lmhead_workspace(n_nodes, hidden_dim, vocab, dtype))
+
+
+def lmhead_argmax(hidden, weight, argmax_ids, max_logit, logits=None, workspace=None, stream=None) -> None:
+    """hidden [N][H]; weight [V][H]; argmax_ids int32 [N]; max_logit float32
+    [N]; logits optional float32 [N][V]."""
+    for t, nm in ((hidden, "hidden"), (weight, "weight"), (argmax_ids, "argmax_ids"), (max_logit, "max_logit")):
+        _dev(t, nm)
+    if logits is not None:
+        _dev(logits, "logits")
+    N, H = hidden.shape
+    V = weight.shape[0]
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().ooo_lmhead_argmax(hidden.data_ptr(), weight.data_ptr(), N, H, V, dtype_code(hidden),
+                                   argmax_ids.data_ptr(), max_logit.data_ptr(), _ptr(logits), _ptr(workspace),
+                                   ws_bytes, _stream(stream)))
+
+
+def accept(token, parent, depth, anc_mask, argmax_ids, n_nodes: int, path, accept_len, bonus_token,
+           stream=None) -> None:
+    """All device int32 tensors (anc_mask int64 [N][W]); path [path_cap]."""
+    for t, nm in ((token, "token"), (parent, "parent"), (depth, "depth"), (anc_mask, "anc_mask"),
+                  (argmax_ids, "argmax_ids"), (path, "path"), (accept_len, "accept_len"),
+                  (bonus_token, "bonus_token")):
+        _dev(t, nm)
+    W = anc_mask.shape[-1]
+    _check(lib().ooo_accept(token.data_ptr(), parent.data_ptr(), depth.data_ptr(), anc_mask.data_ptr(), W,
+                            argmax_ids.data_ptr(), n_nodes, path.numel(), path.data_ptr(), accept_len.data_ptr(),
+                            bonus_token.data_ptr(), _stream(stream)))
+
+
+def kv_compact(k_cache, v_cache, prefix_len: int, n_nodes: int, path, accept_len, stream=None) -> None:
+    """k_cache/v_cache [L][Hkv][cap][D] contiguous, updated in place."""
+    for t, nm in ((k_cache, "k_cache"), (v_cache, "v_cache"), (path, "path"), (accept_len, "accept_len")):
+        _dev(t, nm)
+    L, Hkv, cap, D = k_cache.shape
+    _check(lib().ooo_kv_compact(k_cache.data_ptr(), v_cache.data_ptr(), L, Hkv, cap, D, dtype_code(k_cache),
+                                prefix_len, n_nodes, path.data_ptr(), accept_len.data_ptr(), path.numel(),
+                                _stream(stream)))

@@ -1,0 +1,143 @@
+"""One verification step as a sequence of libooo calls.
+
+The runner owns the per-step device buffers (trie arrays, per-layer
+attention outputs, greedy tokens, accepted path, workspaces) for one
+workload shape and issues, on one stream:
+
+    H2D of the packed trie  ->  n_layers x ooo_tree_attn  ->  ooo_lmhead_argmax
+    ->  ooo_accept  ->  ooo_kv_compact  ->  D2H of (L, bonus, path)
+
+Packing runs on the host through ``ooo_pack_tree``.  The node queries, the
+node K/V rows written into the cache and the hidden rows feeding the LM head
+are the model's job (its projections); the caller stages them.
+"""
+
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import ooo
+
+
+@dataclass
+class StepResult:
+    n_nodes: int
+    n_truncated: int
+    L: int
+    bonus: int
+    path: np.ndarray
+
+    @property
+    def committed_count(self) -> int:
+        return self.L + 1
+
+
+class VerifyRunner:
+    def __init__(self, n_layers: int, n_q_heads: int, n_kv_heads: int, head_dim: int, hidden: int, vocab: int,
+                 max_nodes: int, max_depth: int, dtype: torch.dtype, device="cuda", max_prefix: int = 0):
+        self.L_m, self.Hq, self.Hkv, self.D = n_layers, n_q_heads, n_kv_heads, head_dim
+        self.H, self.V = hidden, vocab
+        self.max_nodes, self.max_depth = max_nodes, max_depth
+        self.W = max(1, (max_nodes + 63) // 64)
+        self.dtype = dtype
+        self.device = torch.device(device)
+        self.code = ooo.BF16 if dtype == torch.bfloat16 else ooo.F32
+        dev = self.device
+        self.path_cap = max_depth + 1
+        # trie on the device, filled from pinned host staging
+        self.h_tree = torch.zeros(3 * max_nodes + 2 * max_nodes * self.W, dtype=torch.int32).pin_memory()
+        self.d_tree = torch.zeros_like(self.h_tree, device=dev)
+        n = max_nodes
+        m = 2 * n * self.W  # mask first so its int64 view stays 8-byte aligned
+        self.mask = self.d_tree[0:m].view(torch.int64).view(n, self.W)
+        self.token = self.d_tree[m:m + n]
+        self.parent = self.d_tree[m + n:m + 2 * n]
+        self.depth = self.d_tree[m + 2 * n:m + 3 * n]
+        self.out = torch.empty(n_layers, max_nodes, n_q_heads, head_dim, dtype=dtype, device=dev)
+        self.ids = torch.empty(max_nodes, dtype=torch.int32, device=dev)
+        self.max_logit = torch.empty(max_nodes, dtype=torch.float32, device=dev)
+        self.res = torch.zeros(2 + self.path_cap, dtype=torch.int32, device=dev)  # L, bonus, path
+        self.accept_len = self.res[0:1]
+        self.bonus = self.res[1:2]
+        self.path = self.res[2:]
+        self.h_res = torch.zeros_like(self.res, device="cpu").pin_memory()
+        self.attn_ws = torch.empty(64, dtype=torch.float32, device=dev)
+        for nn in sorted({1, max(1, max_nodes // 2), max_nodes}):
+            self.ensure_workspace(max(max_prefix, 1), nn)
+        lws = ooo.lmhead_workspace(max_nodes, hidden, vocab, self.code)
+        self.lm_ws = torch.empty(max(lws, 256) // 4 + 1, dtype=torch.float32, device=dev)
+        self.scale = 1.0 / math.sqrt(head_dim)
+        self.n_nodes = 0
+        self.packed = None
+
+    # -- host ---------------------------------------------------------------
+    def pack(self, root_token: int, cand_tokens: np.ndarray, cand_offsets: np.ndarray) -> dict:
+        p = ooo.pack_tree(root_token, cand_tokens, cand_offsets, self.max_nodes, self.max_depth, self.W)
+        n = self.max_nodes
+        m = 2 * n * self.W
+        h = self.h_tree.numpy()
+        k = p["n_nodes"]
+        h[0:m].view(np.uint64).reshape(n, self.W)[:k] = p["anc_mask"]
+        h[m:m + k] = p["token"]
+        h[m + n:m + n + k] = p["parent"]
+        h[m + 2 * n:m + 2 * n + k] = p["depth"]
+        self.n_nodes = k
+        self.packed = p
+        return p
+
+    def ensure_workspace(self, prefix_len: int, n_nodes: Optional[int] = None) -> None:
+        """Grow the attention workspace (outside any timed or captured region)."""
+        n = self.n_nodes if n_nodes is None else n_nodes
+        need = ooo.tree_attn_workspace(max(n, 1), self.Hq, self.Hkv, self.D, prefix_len, self.code)
+        if need > self.attn_ws.numel() * 4:
+            self.attn_ws = torch.empty(need // 4 + 1, dtype=torch.float32, device=self.device)
+
+    # -- device -------------------------------------------------------------
+    def upload_tree(self, stream=None) -> None:
+        self.d_tree.copy_(self.h_tree, non_blocking=True)
+
+    def attention(self, layer: int, q, k_layer, v_layer, prefix_len: int, stream=None) -> None:
+        N = self.n_nodes
+        ooo.tree_attn(q, k_layer, v_layer, prefix_len, N, self.mask[:N], self.Hq, self.Hkv, self.scale,
+                      self.out[layer, :N], self.attn_ws, stream)
+
+    def lm_head(self, hidden, logits=None, stream=None) -> None:
+        N = self.n_nodes
+        ooo.lmhead_argmax(hidden[:N], self._weight, self.ids[:N], self.max_logit[:N], logits, self.lm_ws, stream)
+
+    def accept(self, stream=None) -> None:
+        N = self.n_nodes
+        ooo.accept(self.token[:N], self.parent[:N], self.depth[:N], self.mask[:N], self.ids[:N], N, self.path,
+                   self.accept_len, self.bonus, stream)
+
+    def compact(self, k_cache, v_cache, prefix_len: int, stream=None) -> None:
+        ooo.kv_compact(k_cache, v_cache, prefix_len, self.n_nodes, self.path, self.accept_len, stream)
+
+    def download(self) -> None:
+        self.h_res.copy_(self.res, non_blocking=True)
+
+    def result(self) -> StepResult:
+        r = self.h_res.numpy()
+        L = int(r[0])
+        return StepResult(self.n_nodes, int(self.packed["n_truncated"]) if self.packed else 0, L, int(r[1]),
+                          r[2:2 + L + 1].copy())
+
+    def set_weight(self, weight) -> None:
+        self._weight = weight
+
+    def device_step(self, q_layers: Sequence, k_cache, v_cache, hidden, prefix_len: int,
+                    logits=None, compact: bool = True) -> None:
+        """Everything after packing, enqueued on the current stream."""
+        self.upload_tree()
+        for l in range(self.L_m):
+            self.attention(l, q_layers[l], k_cache[l], v_cache[l], prefix_len)
+        self.lm_head(hidden, logits)
+        self.accept()
+        if compact:
+            self.compact(k_cache, v_cache, prefix_len)
+        self.download()
