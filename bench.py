@@ -1,0 +1,285 @@
+"""Verify-step throughput of the tree-verification path on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload qwen3-8b] [--cpu-seconds S]
+
+A step is one whole verification pass over one batch of synthetic input at
+the Qwen3-8B shape (36 layers, 32 query / 8 KV heads, head_dim 128, 4096
+committed prefix rows, 64-node trie, hidden 4096, vocabulary 151936, bf16):
+
+  host   ooo_pack_tree of the step's candidates (hint, FSM chain, 2 retrieved)
+  graph  H2D of the packed trie; the node K/V rows written into cache rows
+         [P, P+N) of every layer (the model's projection output, staged from
+         a resident copy); 36 x ooo_tree_attn
+  eager  ooo_lmhead_argmax, bracketed by HIP events on its stream
+  graph  ooo_accept, ooo_kv_compact, D2H of (L, bonus, path)
+  host   stream synchronise and read the accepted length (the next step's
+         candidates depend on it in a real decode loop)
+
+All inputs are resident in HBM before timing starts.  Prints one JSON line.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "verify steps/s + tree-attn/LM-head HBM GB/s, Qwen3-8B shape, 64-node trie, 4k ctx"
+
+
+def attention_bytes(cfg, N):
+    """Algorithmic HBM bytes of one layer: K/V prefix + K/V of the nodes + Q + O."""
+    e = cfg.elt_bytes
+    kv = 2 * cfg.n_kv_heads * (cfg.prefix_len + N) * cfg.head_dim * e
+    qo = 2 * N * cfg.n_q_heads * cfg.head_dim * e
+    return kv + qo
+
+
+def lmhead_bytes(cfg, N):
+    """W + X + greedy ids and max logits."""
+    e = cfg.elt_bytes
+    return cfg.vocab * cfg.hidden * e + N * cfg.hidden * e + N * 8
+
+
+def cpu_baseline(cfg, seconds: float):
+    """Time the CPU reference on whole verification steps of the same
+    workload until about ``seconds`` have passed (at least one step)."""
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    from oracle import tree_verify as ov
+    from paper_2608_00814_amd import workload as wl
+
+    seed = 0
+    cands = wl.candidates_for(cfg, seed, 0)
+    tree = ov.pack_tree(cands.root_token, cands.seqs, cands.max_nodes, cands.max_depth)
+    N = tree["n_nodes"]
+    tau, _ = wl.designated_tokens(cfg, seed, 0, cands, tree["token"], tree["parent"])
+    w_st = wl.lm_head_weight(cfg, seed)
+    x64 = wl.to_f64(wl.hidden_rows(cfg, seed, 0, w_st, tau, N), cfg.dtype)
+    w64 = wl.to_f32(w_st, cfg.dtype)  # exact; the reference widens it to float64 chunk by chunk
+    del w_st
+    layers = []
+    for l in range(cfg.n_layers):
+        k, v = wl.layer_cache(cfg, seed, l, N)
+        layers.append((wl.to_f64(wl.queries(cfg, seed, 0, l, N), cfg.dtype), wl.to_f64(k, cfg.dtype),
+                       wl.to_f64(v, cfg.dtype)))
+    steps = 0
+    t0 = time.perf_counter()
+    while True:
+        res = ov.verify_step(cands.root_token, cands.seqs, cands.max_nodes, cands.max_depth, layers,
+                             cfg.prefix_len, cfg.n_kv_heads, x64, w64)
+        kc = [l[1] for l in layers]
+        vc = [l[2] for l in layers]
+        ov.kv_compact(kc + vc, cfg.prefix_len, res["path"])
+        steps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    return {"value": steps / el, "unit": "verify steps/s", "cores": threads, "kind": "oracle",
+            "sample": f"{steps} whole {cfg.name} verify step(s) (pack, {cfg.n_layers}-layer tree attention, "
+                      f"LM head, accept, compact) in fp64 NumPy, {el:.1f} s, on {platform.processor() or 'host'} "
+                      f"with {threads} BLAS threads"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="qwen3-8b")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true", help="launch every kernel eagerly")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for {args.gpus}); the path runs on a single MI355X.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2608_00814_amd import ooo
+    from paper_2608_00814_amd import workload as wl
+    from paper_2608_00814_amd.step import VerifyRunner
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a ROCm GPU", file=sys.stderr)
+        sys.exit(1)
+    ooo.lib()  # fail loudly if the native library is missing
+    cfg = wl.CONFIGS[args.workload]
+    dev = torch.device("cuda:0")
+    tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    P = cfg.prefix_len
+    t_setup = time.time()
+
+    def up(a):
+        if cfg.dtype == "bf16":
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+
+    # --- resident inputs ---------------------------------------------------
+    n_variants = 4  # distinct candidate sets, cycled over the timed steps
+    cand_sets = [wl.candidates_for(cfg, s, 0) for s in range(n_variants)]
+    runner = VerifyRunner(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.hidden, cfg.vocab,
+                          cfg.max_nodes, cfg.max_depth, tdt, dev, max_prefix=P)
+    csr = [c.csr() for c in cand_sets]
+    packs = [runner.pack(c.root_token, *x) for c, x in zip(cand_sets, csr)]
+    N = packs[0]["n_nodes"]
+    assert all(p["n_nodes"] == N for p in packs)
+    w = wl.lm_head_weight(cfg, 0)
+    w_dev = up(w)
+    runner.set_weight(w_dev)
+    hid = []
+    for s, (c, p) in enumerate(zip(cand_sets, packs)):
+        tau, _ = wl.designated_tokens(cfg, s, 0, c, p["token"], p["parent"])
+        hid.append(up(wl.hidden_rows(cfg, s, 0, w, tau, N)))
+    del w
+    shp = (cfg.n_layers, cfg.n_kv_heads, cfg.cap, cfg.head_dim)
+    k_cache = torch.zeros(shp, dtype=tdt, device=dev)
+    v_cache = torch.zeros(shp, dtype=tdt, device=dev)
+    k_nodes = torch.empty(cfg.n_layers, cfg.n_kv_heads, N, cfg.head_dim, dtype=tdt, device=dev)
+    v_nodes = torch.empty_like(k_nodes)
+    q_layers = []
+    for l in range(cfg.n_layers):
+        kc, vc = wl.layer_cache(cfg, 0, l, N)
+        k_cache[l].copy_(up(kc))
+        v_cache[l].copy_(up(vc))
+        k_nodes[l].copy_(k_cache[l, :, P:P + N])
+        v_nodes[l].copy_(v_cache[l, :, P:P + N])
+        q_layers.append(up(wl.queries(cfg, 0, 0, l, N)))
+    hidden = torch.empty_like(hid[0])
+    runner.ensure_workspace(P)
+    torch.cuda.synchronize()
+    setup_s = time.time() - t_setup
+
+    stream = torch.cuda.Stream()  # default priority
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+
+    def stage_and_attend():
+        runner.upload_tree()
+        k_cache[:, :, P:P + N].copy_(k_nodes)
+        v_cache[:, :, P:P + N].copy_(v_nodes)
+        for l in range(cfg.n_layers):
+            runner.attention(l, q_layers[l], k_cache[l], v_cache[l], P)
+
+    def tail():
+        runner.accept()
+        runner.compact(k_cache, v_cache, P)
+        runner.download()
+
+    graphs = None
+    with torch.cuda.stream(stream):
+        runner.pack(cand_sets[0].root_token, *csr[0])
+        hidden.copy_(hid[0])
+        if not args.no_graph:
+            # eager warm-up of every kernel before capture
+            stage_and_attend()
+            runner.lm_head(hidden)
+            tail()
+            stream.synchronize()
+            ga, gt = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+            with torch.cuda.graph(ga, stream=stream):
+                stage_and_attend()
+            with torch.cuda.graph(gt, stream=stream):
+                tail()
+            graphs = (ga, gt)
+        stream.synchronize()
+
+        lm_ms, attn_ms, Ls = [], [], []
+
+        def one_step(i, timed):
+            v = i % n_variants
+            runner.pack(cand_sets[v].root_token, *csr[v])
+            hidden.copy_(hid[v])
+            ev[0].record(stream)
+            if graphs:
+                graphs[0].replay()
+            else:
+                stage_and_attend()
+            ev[1].record(stream)
+            runner.lm_head(hidden)
+            ev[2].record(stream)
+            if graphs:
+                graphs[1].replay()
+            else:
+                tail()
+            stream.synchronize()
+            r = runner.result()
+            if timed:
+                Ls.append(r.L)
+                attn_ms.append(ev[0].elapsed_time(ev[1]))
+                lm_ms.append(ev[1].elapsed_time(ev[2]))
+            return r
+
+        for i in range(args.warmup):
+            one_step(i, False)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            one_step(i, True)
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+
+    ms_per_step = 1e3 * elapsed / args.steps
+    steps_per_s = args.steps / elapsed
+    tokens_per_s = float(np.sum(np.array(Ls) + 1)) / elapsed
+    lm_us = 1e3 * float(np.mean(lm_ms))
+    attn_stage_us = 1e3 * float(np.mean(attn_ms))
+    stage_bytes = 2 * 2 * cfg.n_layers * cfg.n_kv_heads * N * cfg.head_dim * cfg.elt_bytes  # read+write K,V nodes
+    a_bytes = attention_bytes(cfg, N)
+    lm_b = lmhead_bytes(cfg, N)
+    lm_gbs = lm_b / (lm_us * 1e-6) / 1e9
+    path_gbs = (cfg.n_layers * a_bytes + lm_b) / ((attn_stage_us + lm_us) * 1e-6) / 1e9
+
+    out = {
+        "metric": METRIC,
+        "value": round(steps_per_s, 2),
+        "unit": "verify steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {cfg.description}", "n_layers": cfg.n_layers,
+                   "q_heads": cfg.n_q_heads, "kv_heads": cfg.n_kv_heads, "head_dim": cfg.head_dim,
+                   "prefix_len": P, "trie_nodes": N, "hidden": cfg.hidden, "vocab": cfg.vocab,
+                   "launch": "eager" if args.no_graph else "hip-graph per phase, LM head eager"},
+        "tokens_per_s": round(tokens_per_s, 1),
+        "mean_accepted_plus_bonus": round(float(np.mean(np.array(Ls) + 1)), 3),
+        "lmhead_us": round(lm_us, 2),
+        "attention_us_per_step": round(attn_stage_us, 2),
+        "attention_us_per_layer": round(attn_stage_us / cfg.n_layers, 3),
+        "path_hbm_gbs": round(path_gbs, 1),
+        "path_hbm_frac": round(path_gbs / HBM_PEAK_GBS, 4),
+        "roofline": {"bound": "hbm", "kernel": "lmhead_bf16_kernel (+ finalize)", "achieved": round(lm_gbs, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(lm_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": None, "bytes_per_launch": lm_b},
+        "setup_s": round(setup_s, 1),
+        "notes": f"attention_us_per_step includes the trie H2D and the node K/V staging ({stage_bytes} bytes)",
+    }
+    if not args.no_cpu_baseline:
+        del k_cache, v_cache, w_dev
+        torch.cuda.empty_cache()
+        out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -24,6 +24,8 @@
 #include <math.h>
 #include <stdlib.h>
 
+#include <type_traits>
+
 #include "device_common.h"
 #include "ooo_internal.h"
 
@@ -52,22 +54,50 @@ struct AttnArgs {
 // consecutive keys per lane and k-step
 __device__ __forceinline__ int sigma(int c) { return (c & ~0xC) | ((c & 4) << 1) | ((c & 8) >> 1); }
 
-template <int D, int WAVES>
-__global__ __launch_bounds__(64 * WAVES) void tree_attn_bf16_kernel(AttnArgs a) {
-  constexpr int NT = 64 * WAVES;
-  constexpr int BM = 32 * WAVES;
-  constexpr int KLD = D + 8;       // K tile row stride (elements)
-  constexpr int VLD = kTile + 8;   // V^T tile row stride (elements)
-  constexpr int K_ELEMS = kTile * KLD;
-  constexpr int V_ELEMS = D * VLD;
-  constexpr int STAGE = K_ELEMS + V_ELEMS;
-  constexpr int KCH = D / 8;                 // 16-byte chunks per row
-  constexpr int K_ITEMS = kTile * KCH;
-  constexpr int KI = K_ITEMS / NT;
-  constexpr int V_ITEMS = (kTile / 4) * KCH; // (4-key group, chunk)
-  constexpr int VI = (V_ITEMS + NT - 1) / NT;
-  static_assert(K_ITEMS % NT == 0, "K staging must divide evenly");
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * STAGE];
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+#define OOO_LDS(p) ((__attribute__((address_space(3))) void*)(p))
+#define OOO_GLB(p) ((const __attribute__((address_space(1))) void*)(p))
+
+// Workgroup barrier without the memory-model fence __syncthreads() adds: the
+// fence would make the loader wave wait for every in-flight LDS DMA.  The
+// "memory" clobber keeps the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// s_waitcnt vmcnt(n) (n <= 63), leaving the other counters alone.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x0F70);
+}
+
+// LDS ring geometry for one head_dim.  A tile is 64 rows of K and 64 rows of
+// V, each row D bf16 values = D/8 16-byte chunks, stored row-major with
+// chunk c of row r at position c ^ (r % (D/8)).  One 1 KiB DMA instruction
+// copies whole contiguous rows (coalesced in global memory); the XOR
+// swizzle makes reads of one chunk down many rows hit distinct banks.  K
+// tiles of all stages come first, then the V tiles, then the block's
+// queries (padded rows, written once), so every LDS read is a per-lane
+// offset plus a compile-time immediate below 64 KiB.
+template <int D>
+struct Ring {
+  static constexpr int CH = D / 8;           // chunks per row
+  static constexpr int ROWB = 2 * D;         // bytes per row
+  static constexpr int MAT = kTile * ROWB;   // bytes of one K or V tile
+  static constexpr int NS = 3;               // stages
+  static constexpr int VREG = NS * MAT;      // start of the V tiles
+  static constexpr int QREG = 2 * NS * MAT;  // start of the queries
+  static constexpr int QLD = ROWB + 16;      // padded query row
+  static constexpr int DMA_MAT = MAT / 1024; // DMA instructions per matrix
+  static constexpr int RPI = 1024 / ROWB;    // rows per DMA instruction
+  static_assert(2 * DMA_MAT <= 63, "vmcnt range");
+};
+
+template <int D, int CW>
+__global__ __launch_bounds__(64 * (CW + 2)) __attribute__((amdgpu_waves_per_eu(1, 2)))
+void tree_attn_bf16_kernel(AttnArgs a) {
+  using R = Ring<D>;
+  constexpr int BM = 32 * CW;  // query rows per block
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[R::QREG + BM * R::QLD];
 
   const int total = a.Hkv * a.row_blocks * a.splits;
   int w = blockIdx.x;
@@ -78,9 +108,47 @@ __global__ __launch_bounds__(64 * WAVES) void tree_attn_bf16_kernel(AttnArgs a) 
   const int g = w / a.row_blocks;
   const int t_begin = (int)((long long)s * a.tiles_total / a.splits);
   const int t_end = (int)((long long)(s + 1) * a.tiles_total / a.splits);
+  const int ntiles = t_end - t_begin;  // >= 1 because splits <= tiles
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+
+  if (wave >= CW) {
+    // ------------------------------------------------- loaders: K (CW), V (CW+1)
+    const bool is_v = wave == CW + 1;
+    const uint16_t* src = (is_v ? a.v : a.k) + (size_t)g * a.cap * D;
+    uint8_t* dst0 = lds + (is_v ? R::VREG : 0);
+    auto issue = [&](int t, int stage) {
+      int row0, limit;
+      if (t < a.tiles_prefix) {
+        row0 = t * kTile;
+        limit = a.P;
+      } else {
+        row0 = a.P + (t - a.tiles_prefix) * kTile;
+        limit = a.P + a.N;
+      }
+      uint8_t* dst = dst0 + stage * R::MAT;
+#pragma unroll
+      for (int j = 0; j < R::DMA_MAT; ++j) {
+        // lane = (row within the instruction, swizzled chunk); rows past the
+        // limit re-read the last valid row (masked keys, zero probability)
+        const int r = j * R::RPI + lane / R::CH;
+        const int c = (lane % R::CH) ^ (r % R::CH);
+        const size_t off = (size_t)min(row0 + r, limit - 1) * D + c * 8;
+        __builtin_amdgcn_global_load_lds(OOO_GLB(src + off), OOO_LDS(dst + j * 1024), 16, 0, 0);
+      }
+    };
+    issue(t_begin, 0);
+    if (ntiles > 1) issue(t_begin + 1, 1);
+    for (int i = 0; i < ntiles; ++i) {
+      if (i + 1 < ntiles) wait_vmcnt<R::DMA_MAT>();  // tile i landed, i+1 may be in flight
+      else wait_vmcnt<0>();
+      wg_barrier();
+      if (i + 2 < ntiles) issue(t_begin + i + 2, (i + 2) % R::NS);
+    }
+    return;
+  }
+
+  // ------------------------------------------------------------------ compute
   const int c = lane & 31, u = lane >> 5;
   const int row = rb * BM + wave * 32 + c;
   const bool row_ok = row < a.M;
@@ -88,168 +156,158 @@ __global__ __launch_bounds__(64 * WAVES) void tree_attn_bf16_kernel(AttnArgs a) 
   const int node = rr / a.G;
   const int head = g * a.G + (rr - node * a.G);
 
-  bf16x8 qf[D / 16];
+  // this wave's 32 query rows into its private LDS slice (padded rows)
+  const uint32_t qb = R::QREG + (wave * 32 + c) * R::QLD + u * 16;  // + 32*dk
   {
     const uint16_t* qrow = a.q + ((size_t)node * a.Hq + head) * D;
 #pragma unroll
-    for (int dk = 0; dk < D / 16; ++dk) qf[dk] = as_bf16x8(ld16(qrow + 16 * dk + 8 * u));
+    for (int dk = 0; dk < D / 16; ++dk)
+      *reinterpret_cast<u32x4*>(lds + qb + 32 * dk) = ld16(qrow + 16 * dk + 8 * u);
   }
-  const uint16_t* kbase = a.k + (size_t)g * a.cap * D;
-  const uint16_t* vbase = a.v + (size_t)g * a.cap * D;
+  // ancestor-mask word of the next tree tile this split will see
+  int next_tt = t_begin > a.tiles_prefix ? t_begin - a.tiles_prefix : 0;
+  uint64_t mnext = a.mask[(size_t)node * a.W + next_tt];
 
-  u32x4 kreg[KI];
-  u32x4 vreg[VI][4];
-
-  auto tile_rows = [&](int t, int& row0, int& limit) {
-    if (t < a.tiles_prefix) {
-      row0 = t * kTile;
-      limit = a.P;
-    } else {
-      row0 = a.P + (t - a.tiles_prefix) * kTile;
-      limit = a.P + a.N;
+  // per-lane LDS byte offsets (loop invariant).  K fragment (half kt, k-step
+  // dk): chunk 2dk+u of row sigma(c)+32kt.  V^T transpose-read source (for
+  // column block dt, key step ks, half h): row 16ks+4h+8(g16/2)+li/4, columns
+  // 32dt+16(g16%2)+4(li%4) .. +3.
+  const int krow = sigma(c);
+  uint32_t koff[D / 16];
+#pragma unroll
+  for (int dk = 0; dk < D / 16; ++dk) koff[dk] = krow * R::ROWB + (((2 * dk + u) ^ (krow % R::CH)) << 4);
+  const int g16 = lane >> 4, li = lane & 15;
+  uint32_t voff[D / 32][2];
+#pragma unroll
+  for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int vr = 4 * h + 8 * (g16 >> 1) + (li >> 2);  // key row within a 16-row block
+      const int col = 32 * dt + 16 * (g16 & 1) + 4 * (li & 3);
+      voff[dt][h] = R::VREG + vr * R::ROWB + (((col >> 3) ^ (vr % R::CH)) << 4) + (col & 7) * 2;
     }
-  };
-
-  auto load_tile = [&](int t) {
-    int row0, limit;
-    tile_rows(t, row0, limit);
-#pragma unroll
-    for (int i = 0; i < KI; ++i) {
-      const int item = tid + i * NT;
-      const int r = item / KCH, ch = item % KCH;
-      const int grow = row0 + r;
-      kreg[i] = grow < limit ? ld16(kbase + (size_t)grow * D + ch * 8) : u32x4{0, 0, 0, 0};
-    }
-#pragma unroll
-    for (int i = 0; i < VI; ++i) {
-      const int item = tid + i * NT;
-      const int kg = item % 16, dch = item / 16;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int grow = row0 + 4 * kg + r;
-        vreg[i][r] = (item < V_ITEMS && grow < limit) ? ld16(vbase + (size_t)grow * D + dch * 8)
-                                                       : u32x4{0, 0, 0, 0};
-      }
-    }
-  };
-
-  auto store_tile = [&](int stage) {
-    uint16_t* Kl = lds + stage * STAGE;
-    uint16_t* Vl = Kl + K_ELEMS;
-#pragma unroll
-    for (int i = 0; i < KI; ++i) {
-      const int item = tid + i * NT;
-      const int r = item / KCH, ch = item % KCH;
-      st16(Kl + r * KLD + ch * 8, kreg[i]);
-    }
-#pragma unroll
-    for (int i = 0; i < VI; ++i) {
-      const int item = tid + i * NT;
-      if (item < V_ITEMS) {
-        const int kg = item % 16, dch = item / 16;
-#pragma unroll
-        for (int p = 0; p < 4; ++p) {
-          const uint32_t x0 = vreg[i][0][p], x1 = vreg[i][1][p], x2 = vreg[i][2][p], x3 = vreg[i][3][p];
-          u32x2 even, odd;  // d = 8*dch + 2p (low halves) and + 1 (high halves)
-          even[0] = (x0 & 0xFFFFu) | (x1 << 16);
-          even[1] = (x2 & 0xFFFFu) | (x3 << 16);
-          odd[0] = (x0 >> 16) | (x1 & 0xFFFF0000u);
-          odd[1] = (x2 >> 16) | (x3 & 0xFFFF0000u);
-          *reinterpret_cast<u32x2*>(Vl + (8 * dch + 2 * p) * VLD + 4 * kg) = even;
-          *reinterpret_cast<u32x2*>(Vl + (8 * dch + 2 * p + 1) * VLD + 4 * kg) = odd;
-        }
-      }
-    }
-  };
 
   f32x16 oacc[D / 32];
 #pragma unroll
   for (int dt = 0; dt < D / 32; ++dt) oacc[dt] = f32x16{};
   float m_run = -INFINITY, l_run = 0.f;
-  const int krow = sigma(c);
 
-  if (t_begin < t_end) {
-    load_tile(t_begin);
-    store_tile(0);
-  }
-  __syncthreads();
+  auto tile = [&](int i, auto stage_c) {
+    constexpr int ST = decltype(stage_c)::value;
+    const int t = t_begin + i;
+    wg_barrier();  // tile t is in stage ST
+    const uint8_t* Ks = lds + ST * R::MAT;
 
-  for (int t = t_begin; t < t_end; ++t) {
-    const int stage = (t - t_begin) & 1;
-    if (t + 1 < t_end) load_tile(t + 1);
-    const uint16_t* Kl = lds + stage * STAGE;
-    const uint16_t* Vl = Kl + K_ELEMS;
-
-    // S^T = K Q^T for 64 keys x 32 rows (two 32-key halves)
-    f32x16 s0 = f32x16{}, s1 = f32x16{};
+    // S^T = K Q^T for both 32-key halves first, so the softmax of half A
+    // (VALU) can run while the matrix cores still work on half B.
+    f32x16 sh[2] = {f32x16{}, f32x16{}};
 #pragma unroll
-    for (int dk = 0; dk < D / 16; ++dk) {
-      const bf16x8 k0 = as_bf16x8(ld16(Kl + krow * KLD + 16 * dk + 8 * u));
-      const bf16x8 k1 = as_bf16x8(ld16(Kl + (32 + krow) * KLD + 16 * dk + 8 * u));
-      s0 = mfma32(k0, qf[dk], s0);
-      s1 = mfma32(k1, qf[dk], s1);
-    }
-    // lane's value j of half h is key 32h + 16*(j/8) + 8u + j%8 of the tile
-    float sv[32];
+    for (int b4 = 0; b4 < D / 64; ++b4) {
+      bf16x8 k0[4], k1[4], qq[4];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      sv[j] = s0[j] * a.scale_log2e;
-      sv[16 + j] = s1[j] * a.scale_log2e;
+      for (int j = 0; j < 4; ++j) {
+        const int dk = 4 * b4 + j;
+        qq[j] = as_bf16x8(*reinterpret_cast<const u32x4*>(lds + qb + 32 * dk));
+        k0[j] = as_bf16x8(*reinterpret_cast<const u32x4*>(Ks + koff[dk]));
+        k1[j] = as_bf16x8(*reinterpret_cast<const u32x4*>(Ks + koff[dk] + 32 * R::ROWB));
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        sh[0] = mfma32(k0[j], qq[j], sh[0]);
+        sh[1] = mfma32(k1[j], qq[j], sh[1]);
+      }
     }
-    int row0, limit;
-    tile_rows(t, row0, limit);
     const bool tree = t >= a.tiles_prefix;
-    if (tree || row0 + kTile > limit) {
-      uint64_t mw = ~0ull;
-      if (tree) {
-        const int word = (row0 - a.P) / 64;
-        mw = a.mask[(size_t)node * a.W + word];
-      }
-#pragma unroll
-      for (int j = 0; j < 32; ++j) {
-        const int off = 16 * (j / 8) + 8 * u + (j % 8);
-        const bool ok = (row0 + off < limit) && ((mw >> off) & 1ull);
-        if (!ok) sv[j] = -INFINITY;
-      }
+    const int row0 = tree ? a.P + (t - a.tiles_prefix) * kTile : t * kTile;
+    const int limit = tree ? a.P + a.N : a.P;
+    const bool masked = tree || row0 + kTile > limit;
+    uint64_t mw = ~0ull;
+    if (tree) {
+      mw = mnext;
+      next_tt = min(next_tt + 1, a.W - 1);
+      mnext = a.mask[(size_t)node * a.W + next_tt];
     }
-    float mx = -INFINITY;
-#pragma unroll
-    for (int j = 0; j < 32; ++j) mx = fmaxf(mx, sv[j]);
-    mx = fmaxf(mx, shfl_xor_f(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = exp2f(m_run - m_use);
-    float psum = 0.f;
-#pragma unroll
-    for (int j = 0; j < 32; ++j) {
-      sv[j] = exp2f(sv[j] - m_use);
-      psum += sv[j];
-    }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int dt = 0; dt < D / 32; ++dt) oacc[dt] *= alpha;
 
-    bf16x8 pf[4];
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      u32x4 pk;
+    for (int hf = 0; hf < 2; ++hf) {
+      // lane's value j of this half is key 32hf + 16*(j/8) + 8u + j%8 of the tile
+      float sv[16];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) pk[e] = pack_bf16x2(sv[8 * ks + 2 * e], sv[8 * ks + 2 * e + 1]);
-      pf[ks] = as_bf16x8(pk);
-    }
-    // O^T += V^T P^T
+      for (int j = 0; j < 16; ++j) sv[j] = sh[hf][j];
+      if (masked) {
 #pragma unroll
-    for (int dt = 0; dt < D / 32; ++dt) {
+        for (int j = 0; j < 16; ++j) {
+          const int off = 32 * hf + 16 * (j / 8) + 8 * u + (j % 8);
+          const bool ok = (row0 + off < limit) && ((mw >> off) & 1ull);
+          if (!ok) sv[j] = -INFINITY;
+        }
+      }
+      float mx = sv[0];
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const bf16x8 vv = as_bf16x8(ld16(Vl + (32 * dt + c) * VLD + 16 * ks + 8 * u));
-        oacc[dt] = mfma32(vv, pf[ks], oacc[dt]);
+      for (int j = 1; j < 16; ++j) mx = __builtin_fmaxf(mx, sv[j]);
+      {
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+        mx = __builtin_fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * a.scale_log2e;  // log2 units
+      }
+      // Lazy rescaling: the reference max m_run moves only when some row of
+      // the wave grows by more than 2^8, so probabilities stay <= 256 (fine
+      // for fp32 sums and bf16 operands) and O, l are rescaled rarely.
+      if (__any(mx > m_run + 8.f)) {
+        const float m_new = __builtin_fmaxf(m_run, mx);
+        const float alpha = __builtin_amdgcn_exp2f(m_run - (m_new == -INFINITY ? 0.f : m_new));
+        l_run *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < D / 32; ++dt) oacc[dt] *= alpha;
+        m_run = m_new;
+      }
+      const float m_use = m_run == -INFINITY ? 0.f : m_run;
+      float psum = 0.f;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        sv[j] = __builtin_amdgcn_exp2f(fmaf(sv[j], a.scale_log2e, -m_use));
+        psum += sv[j];
+      }
+      l_run += psum;
+      bf16x8 pf[2];
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2) {
+        u32x4 pk;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) pk[e] = pack_bf16x2(sv[8 * k2 + 2 * e], sv[8 * k2 + 2 * e + 1]);
+        pf[k2] = as_bf16x8(pk);
+      }
+      // O^T += V^T P^T for this half (key steps ks = 2hf, 2hf+1).  V^T
+      // fragments come from the row-major V tile through the LDS transpose
+      // read: within each 16-lane group, source lane 4k+q points at key row
+      // k, columns 4q..4q+3, and lane i receives column i of the four rows.
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2) {
+        const int ks = 2 * hf + k2;
+        bf16x8 vv[D / 32];
+#pragma unroll
+        for (int dt = 0; dt < D / 32; ++dt) {
+          u32x2 lohi[2];
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const uint8_t* p = lds + voff[dt][h] + ST * R::MAT + ks * 16 * R::ROWB;
+            lohi[h] = __builtin_bit_cast(
+                u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((i16x4 __attribute__((address_space(3)))*)OOO_LDS(p)));
+          }
+          vv[dt] = as_bf16x8(u32x4{lohi[0][0], lohi[0][1], lohi[1][0], lohi[1][1]});
+        }
+#pragma unroll
+        for (int dt = 0; dt < D / 32; ++dt) oacc[dt] = mfma32(vv[dt], pf[k2], oacc[dt]);
       }
     }
-    if (t + 1 < t_end) store_tile(stage ^ 1);
-    __syncthreads();
+  };
+  int i = 0;
+  for (; i + R::NS <= ntiles; i += R::NS) {
+    tile(i, std::integral_constant<int, 0>{});
+    tile(i + 1, std::integral_constant<int, 1>{});
+    tile(i + 2, std::integral_constant<int, 2>{});
   }
+  if (i < ntiles) tile(i, std::integral_constant<int, 0>{});
+  if (i + 1 < ntiles) tile(i + 1, std::integral_constant<int, 1>{});
 
   const float l_tot = l_run + shfl_xor_f(l_run, 32);
   if (!row_ok) return;
@@ -285,7 +343,11 @@ __global__ __launch_bounds__(64 * WAVES) void tree_attn_bf16_kernel(AttnArgs a) 
   }
 }
 
-// Merge the splits of each query row: O = sum_s 2^(m_s - m) O_s / sum_s 2^(m_s - m) l_s.
+// Merge the splits of each query row, online over the splits:
+// O = sum_s 2^(m_s - m) O_s / sum_s 2^(m_s - m) l_s.  A split that saw no
+// allowed key has m_s = -inf, l_s = 0 and O_s = 0 and gets weight zero.
+// Every split's loads are independent of the running state, so the unrolled
+// loop keeps many of them in flight.
 template <int D>
 __global__ __launch_bounds__(256) void tree_attn_combine_kernel(AttnArgs a) {
   constexpr int TPR = D / 4;  // threads per row, 4 columns each
@@ -293,17 +355,21 @@ __global__ __launch_bounds__(256) void tree_attn_combine_kernel(AttnArgs a) {
   if (gr >= a.Hkv * a.M) return;
   const int g = gr / a.M, r = gr % a.M;
   const int d0 = (threadIdx.x % TPR) * 4;
-  float mmax = -INFINITY;
-  for (int s = 0; s < a.splits; ++s) mmax = fmaxf(mmax, a.part_ml[(((size_t)s * a.Hkv + g) * a.Mpad + r) * 2]);
-  float den = 0.f;
+  const size_t stride = (size_t)a.Hkv * a.Mpad;  // rows between consecutive splits
+  const size_t row0 = (size_t)g * a.Mpad + r;
+  float mrun = -INFINITY, den = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
   for (int s = 0; s < a.splits; ++s) {
-    const size_t prow = ((size_t)s * a.Hkv + g) * a.Mpad + r;
-    const float m = a.part_ml[prow * 2];
-    if (m == -INFINITY) continue;
-    const float wgt = exp2f(m - mmax);
-    den += wgt * a.part_ml[prow * 2 + 1];
-    acc += wgt * *reinterpret_cast<const f32x4*>(a.part_o + prow * D + d0);
+    const size_t prow = row0 + s * stride;
+    const float m = a.part_ml[prow * 2], l = a.part_ml[prow * 2 + 1];
+    const f32x4 o = *reinterpret_cast<const f32x4*>(a.part_o + prow * D + d0);
+    const float mn = __builtin_fmaxf(mrun, m);
+    const float base = mn == -INFINITY ? 0.f : mn;
+    const float c_old = __builtin_amdgcn_exp2f(mrun - base), c_new = __builtin_amdgcn_exp2f(m - base);
+    den = den * c_old + l * c_new;
+    acc = acc * c_old + o * c_new;
+    mrun = mn;
   }
   const float inv = 1.f / den;
   const int node = r / a.G, head = g * a.G + r % a.G;
@@ -452,11 +518,11 @@ extern "C" int ooo_tree_attn(const void* q, const void* k_cache, const void* v_c
     }
     const dim3 grid(n_kv_heads * p.row_blocks * p.splits);
     if (head_dim == 128) {
-      if (p.waves == 2) tree_attn_bf16_kernel<128, 2><<<grid, 128, 0, st>>>(a);
-      else tree_attn_bf16_kernel<128, 4><<<grid, 256, 0, st>>>(a);
+      if (p.waves == 2) tree_attn_bf16_kernel<128, 2><<<grid, 256, 0, st>>>(a);
+      else tree_attn_bf16_kernel<128, 4><<<grid, 384, 0, st>>>(a);
     } else {
-      if (p.waves == 2) tree_attn_bf16_kernel<64, 2><<<grid, 128, 0, st>>>(a);
-      else tree_attn_bf16_kernel<64, 4><<<grid, 256, 0, st>>>(a);
+      if (p.waves == 2) tree_attn_bf16_kernel<64, 2><<<grid, 256, 0, st>>>(a);
+      else tree_attn_bf16_kernel<64, 4><<<grid, 384, 0, st>>>(a);
     }
     if (p.splits > 1) {
       const int rows = n_kv_heads * a.M;

@@ -125,20 +125,64 @@ CONFIGS: Dict[str, VerifyConfig] = {
 # number formats
 
 
+def _bf16_round(x: np.ndarray) -> np.ndarray:
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    bias = ((u >> 16) & np.uint32(1)) + np.uint32(0x7FFF)
+    return ((u + bias) >> np.uint32(16)).astype(np.uint16)
+
+
+def _chunked(n: int, fn) -> None:
+    """Run fn(a, b) over [0, n) in chunks on a thread pool."""
+    step = 1 << 22
+    spans = [(a, min(n, a + step)) for a in range(0, n, step)]
+    if len(spans) <= 1:
+        for a, b in spans:
+            fn(a, b)
+        return
+    with ThreadPoolExecutor(_THREADS) as ex:
+        list(ex.map(lambda ab: fn(*ab), spans))
+
+
 def to_bf16_bits(x: np.ndarray) -> np.ndarray:
     """float32 -> bfloat16 bit patterns (uint16), round to nearest even."""
     x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32)
-    bias = ((u >> 16) & 1) + np.uint32(0x7FFF)
-    return ((u + bias) >> 16).astype(np.uint16)
+    out = np.empty(x.shape, dtype=np.uint16)
+    xf, of = x.reshape(-1), out.reshape(-1)
+
+    def fn(a, b):
+        of[a:b] = _bf16_round(xf[a:b])
+
+    _chunked(xf.size, fn)
+    return out
 
 
 def bf16_to_f32(bits: np.ndarray) -> np.ndarray:
-    return (np.ascontiguousarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+    bits = np.ascontiguousarray(bits, dtype=np.uint16)
+    out = np.empty(bits.shape, dtype=np.float32)
+    bf, of = bits.reshape(-1), out.reshape(-1)
+
+    def fn(a, b):
+        of[a:b] = (bf[a:b].astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+    _chunked(bf.size, fn)
+    return out
+
+
+def to_f32(arr: np.ndarray, dtype: str) -> np.ndarray:
+    """Stored values as float32 (exact for bf16 and float32 storage)."""
+    return bf16_to_f32(arr) if dtype == "bf16" else np.asarray(arr, dtype=np.float32)
 
 
 def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
-    return bf16_to_f32(bits).astype(np.float64)
+    bits = np.ascontiguousarray(bits, dtype=np.uint16)
+    out = np.empty(bits.shape, dtype=np.float64)
+    bf, of = bits.reshape(-1), out.reshape(-1)
+
+    def fn(a, b):
+        of[a:b] = (bf[a:b].astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+    _chunked(bf.size, fn)
+    return out
 
 
 def to_f64(arr: np.ndarray, dtype: str) -> np.ndarray:
@@ -166,12 +210,13 @@ _THREADS = max(1, min(16, len(os.sched_getaffinity(0))))
 
 
 def normal(cfg: VerifyConfig, seed: int, step: int, stream: int, shape: Tuple[int, ...],
-           std: float = 1.0, extra: Sequence[int] = ()) -> np.ndarray:
-    """float32 N(0, std^2) array, drawn in independent chunks along axis 0 so
-    large tensors fill on several threads; the values do not depend on the
-    thread count."""
+           std: float = 1.0, extra: Sequence[int] = (), stored: Optional[str] = None) -> np.ndarray:
+    """N(0, std^2) draw in float32, generated in independent chunks along
+    axis 0 on several threads (values do not depend on the thread count).
+    With ``stored="bf16"`` each chunk is rounded to bf16 bits as it is drawn,
+    so the float32 array is never materialised."""
     shape = tuple(int(s) for s in shape)
-    out = np.empty(shape, dtype=np.float32)
+    out = np.empty(shape, dtype=np.uint16 if stored == "bf16" else np.float32)
     if out.size == 0:
         return out
     lead = shape[0]
@@ -182,9 +227,10 @@ def normal(cfg: VerifyConfig, seed: int, step: int, stream: int, shape: Tuple[in
     def fill(ci: int) -> None:
         a, b = chunks[ci]
         g = rng(cfg, seed, step, stream, *extra, ci)
-        out[a:b] = g.standard_normal((b - a,) + shape[1:], dtype=np.float32)
+        x = g.standard_normal((b - a,) + shape[1:], dtype=np.float32)
         if std != 1.0:
-            out[a:b] *= np.float32(std)
+            x *= np.float32(std)
+        out[a:b] = _bf16_round(x) if stored == "bf16" else x
 
     if len(chunks) == 1:
         fill(0)
@@ -192,6 +238,12 @@ def normal(cfg: VerifyConfig, seed: int, step: int, stream: int, shape: Tuple[in
         with ThreadPoolExecutor(_THREADS) as ex:
             list(ex.map(fill, range(len(chunks))))
     return out
+
+
+def draw(cfg: VerifyConfig, seed: int, step: int, stream: int, shape, std: float = 1.0,
+         extra: Sequence[int] = ()) -> np.ndarray:
+    """N(0, std^2) in the workload's stored representation."""
+    return normal(cfg, seed, step, stream, shape, std, extra, stored=cfg.dtype if cfg.dtype == "bf16" else None)
 
 
 # ----------------------------------------------------------------------------
@@ -353,8 +405,7 @@ def designated_tokens(cfg: VerifyConfig, seed: int, step: int, cands: Candidates
 
 def lm_head_weight(cfg: VerifyConfig, seed: int) -> np.ndarray:
     """W[V][H] ~ N(0, 0.02^2), stored in ``cfg.dtype``."""
-    w = normal(cfg, seed, 0, S_LMW, (cfg.vocab, cfg.hidden), std=0.02)
-    return store(w, cfg.dtype)
+    return draw(cfg, seed, 0, S_LMW, (cfg.vocab, cfg.hidden), std=0.02)
 
 
 def hidden_rows(cfg: VerifyConfig, seed: int, step: int, w_stored: np.ndarray,
@@ -376,25 +427,20 @@ def hidden_rows(cfg: VerifyConfig, seed: int, step: int, w_stored: np.ndarray,
 
 def queries(cfg: VerifyConfig, seed: int, step: int, layer: int, n_nodes: int) -> np.ndarray:
     """Q[N][Hq][D] for one layer (post-RoPE stand-in)."""
-    q = normal(cfg, seed, step, S_QUERY, (n_nodes, cfg.n_q_heads, cfg.head_dim), extra=(layer,))
-    return store(q, cfg.dtype)
+    return draw(cfg, seed, step, S_QUERY, (n_nodes, cfg.n_q_heads, cfg.head_dim), extra=(layer,))
 
 
 def prefix_kv(cfg: VerifyConfig, seed: int, layer: int, prefix_len: Optional[int] = None) -> Tuple[np.ndarray, np.ndarray]:
     """Committed prefix rows K,V[Hkv][P][D] of one layer."""
     P = cfg.prefix_len if prefix_len is None else prefix_len
     shp = (cfg.n_kv_heads, P, cfg.head_dim)
-    k = normal(cfg, seed, 0, S_KPRE, shp, extra=(layer,))
-    v = normal(cfg, seed, 0, S_VPRE, shp, extra=(layer,))
-    return store(k, cfg.dtype), store(v, cfg.dtype)
+    return draw(cfg, seed, 0, S_KPRE, shp, extra=(layer,)), draw(cfg, seed, 0, S_VPRE, shp, extra=(layer,))
 
 
 def tree_kv(cfg: VerifyConfig, seed: int, step: int, layer: int, n_nodes: int) -> Tuple[np.ndarray, np.ndarray]:
     """This step's node rows K,V[Hkv][N][D] of one layer (row i = node i)."""
     shp = (cfg.n_kv_heads, n_nodes, cfg.head_dim)
-    k = normal(cfg, seed, step, S_KTREE, shp, extra=(layer,))
-    v = normal(cfg, seed, step, S_VTREE, shp, extra=(layer,))
-    return store(k, cfg.dtype), store(v, cfg.dtype)
+    return draw(cfg, seed, step, S_KTREE, shp, extra=(layer,)), draw(cfg, seed, step, S_VTREE, shp, extra=(layer,))
 
 
 def layer_cache(cfg: VerifyConfig, seed: int, layer: int, n_nodes: int, step: int = 0,

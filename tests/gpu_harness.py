@@ -123,7 +123,7 @@ def run_and_check(name: str, seed: int = 0, layers: Optional[Sequence[int]] = No
         return out
 
     # LM head and greedy tokens
-    ref_logits = ov.lm_head_logits(wl.to_f64(x, dt), wl.to_f64(w, dt))
+    ref_logits = ov.lm_head_logits(wl.to_f64(x, dt), wl.to_f32(w, dt))
     g = ov.greedy_tokens(ref_logits)
     assert g["margin"].min() >= MIN_MARGIN, "input margin below the tie-exclusion bound"
     assert np.array_equal(ids, g["ids"]), (ids, g["ids"])
