@@ -141,7 +141,8 @@ def main():
     assert all(p["n_nodes"] == N for p in packs)
     w = wl.lm_head_weight(cfg, 0)
     w_dev = up(w)
-    runner.set_weight(w_dev)
+    runner.set_weight(w_dev)  # packed once for streaming; not part of a step
+    del w_dev
     hid = []
     for s, (c, p) in enumerate(zip(cand_sets, packs)):
         tau, _ = wl.designated_tokens(cfg, s, 0, c, p["token"], p["parent"])
@@ -275,7 +276,7 @@ def main():
         "notes": f"attention_us_per_step includes the trie H2D and the node K/V staging ({stage_bytes} bytes)",
     }
     if not args.no_cpu_baseline:
-        del k_cache, v_cache, w_dev
+        del k_cache, v_cache
         torch.cuda.empty_cache()
         out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -9,6 +9,7 @@
  *   ooo_tree_attn      per layer: every trie node attends to the committed
  *                      prefix and to its own ancestors (one pass for the tree)
  *   ooo_lmhead_argmax  LM head over all nodes and the greedy token of each
+ *                      (ooo_lmhead_pack lays the weight out for streaming)
  *   ooo_accept         longest root path whose tokens agree with the greedy
  *                      tokens, plus the target's own next (bonus) token
  *   ooo_kv_compact     move the accepted nodes' K/V rows into the committed
@@ -123,26 +124,52 @@ int ooo_tree_attn(const void* q, const void* k_cache, const void* v_cache, int64
                   void* stream);
 
 /*
+ * ooo_lmhead_pack - one-time re-layout of the LM-head weight for streaming.
+ *
+ * The LM head reads all of W once per step and is bound by HBM bandwidth.
+ * In nn.Linear layout each 128-row tile of W is read 128 bytes per row at a
+ * time from rows hidden_dim*2 bytes apart; the packed layout stores each
+ * (128-row tile, 64-column chunk) block as one contiguous 16 KiB run, with
+ * rows past `vocab` zero-filled, so the kernel streams W strictly in order.
+ * Model weights are static, so the packing runs once when the weight is
+ * loaded, not per step.
+ *
+ * DEVICE pointers; OOO_BF16 only; asynchronous on `stream`.
+ *   weight   [vocab][hidden_dim] (nn.Linear layout), read only
+ *   packed   ooo_lmhead_packed_bytes(vocab, hidden_dim, dt) bytes; must not
+ *            alias `weight`
+ * Errors: OOO_ERR_INVALID (null pointers, non-positive sizes),
+ * OOO_ERR_UNSUPPORTED (dtype other than OOO_BF16, hidden_dim % 64 != 0),
+ * OOO_ERR_CAPACITY (packed_bytes too small), OOO_ERR_HIP.
+ */
+typedef enum { OOO_W_ROWS = 0, OOO_W_PACKED = 1 } ooo_weight_layout;
+size_t ooo_lmhead_packed_bytes(int32_t vocab, int32_t hidden_dim, ooo_dtype dt);
+int ooo_lmhead_pack(const void* weight, int32_t vocab, int32_t hidden_dim, ooo_dtype dt, void* packed,
+                    size_t packed_bytes, void* stream);
+
+/*
  * ooo_lmhead_argmax - LM head and greedy token of every node (Eq. 1: the
  * committed token is the target's most likely next token).
  *
  * DEVICE pointers.
  *   hidden     [n_nodes][hidden_dim] final hidden rows
- *   weight     [vocab][hidden_dim] (nn.Linear layout)
+ *   weight     OOO_W_ROWS: [vocab][hidden_dim] (nn.Linear layout);
+ *              OOO_W_PACKED: the output of ooo_lmhead_pack (OOO_BF16 only)
  *   argmax_ids [n_nodes] int32: lowest vocabulary index among equal maxima
  *   max_logit  [n_nodes] float32: the logit at argmax_ids
  *   logits     NULL, or [n_nodes][vocab] float32 (validation dump)
- * Logits are float32 sums of exact products.
+ * Logits are float32 sums of exact products, added in the same order for
+ * every vocabulary row, so identical weight rows give identical logits.
  * Supported: OOO_BF16 needs hidden_dim % 64 == 0 and n_nodes <= 256;
- * OOO_F32 needs hidden_dim % 4 == 0.
- * Errors: OOO_ERR_INVALID (null pointers, non-positive sizes),
- * OOO_ERR_UNSUPPORTED, OOO_ERR_CAPACITY, OOO_ERR_HIP.
+ * OOO_F32 needs hidden_dim % 4 == 0 and the OOO_W_ROWS layout.
+ * Errors: OOO_ERR_INVALID (null pointers, non-positive sizes, unknown
+ * layout), OOO_ERR_UNSUPPORTED, OOO_ERR_CAPACITY, OOO_ERR_HIP.
  */
 size_t ooo_lmhead_workspace(int32_t n_nodes, int32_t hidden_dim, int32_t vocab, ooo_dtype dt);
 int ooo_lmhead_argmax(const void* hidden, const void* weight, int32_t n_nodes,
-                      int32_t hidden_dim, int32_t vocab, ooo_dtype dt, int32_t* argmax_ids,
-                      float* max_logit, float* logits, void* workspace, size_t ws_bytes,
-                      void* stream);
+                      int32_t hidden_dim, int32_t vocab, ooo_dtype dt, int32_t weight_layout,
+                      int32_t* argmax_ids, float* max_logit, float* logits, void* workspace,
+                      size_t ws_bytes, void* stream);
 
 /*
  * ooo_accept - longest greedy-agreeing root path (Section 4.4, Verify and

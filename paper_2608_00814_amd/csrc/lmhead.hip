@@ -2,20 +2,21 @@
 // token is the target's most likely one; ties go to the lowest index).
 //
 // bf16 path: the product is W[V][H] x X[N][H]^T, a skinny GEMM that streams
-// W from HBM once.  Each wave owns 32*RA vocabulary rows and all nodes in
-// 32*NB columns, accumulating logits^T tiles on the matrix cores:
-//  * A operand = W rows, B operand = X rows, both read straight from global
-//    memory into registers (X is small and stays in L1/L2).
-//  * The contraction index is permuted inside each 64-element chunk so a
-//    lane reads 64 contiguous bytes of its row per chunk: MFMA k-step s,
-//    lane half u, element e covers k = 32u + 8s + e.  The sum over k does
-//    not depend on the order, and A and B use the same permutation.
-//  * Chunks are double-buffered in registers so the next chunk's loads are
-//    in flight while the current one is multiplied.
-//  * Each lane ends with 16*RA logits of one node; the per-node argmax is
-//    reduced in registers, across the two lane halves, across the block's
-//    waves in LDS, and across blocks by a small finalize kernel reading the
-//    per-block winners (deterministic: value, then lowest index).
+// W from HBM once; it is bound by HBM bandwidth, so the design is about
+// keeping enough whole cache lines in flight:
+//  * A persistent grid (one block per CU) walks 128-row vocabulary tiles
+//    round-robin; the K dimension is cut into 64-element chunks.
+//  * Two loader waves copy each chunk of W (128 rows x 128 B) and of X
+//    (all nodes x 128 B) from global memory straight into a 3-5 stage LDS
+//    ring with global_load_lds: every DMA instruction moves 8 whole rows.
+//    The 16-byte pieces of a row are XOR-swizzled by (row % 8).
+//  * Four compute waves own 32 rows each and read A (W) and B (X) MFMA
+//    fragments from LDS; they never issue global loads in the loop.
+//  * The contraction index inside a chunk follows the pieces: MFMA k-step s,
+//    lane half u, element e is k = 8 * (2s + u) + e for both operands.
+//  * Each lane ends a tile with 16 logits of one node; the per-node argmax is
+//    kept in registers across tiles, merged across the block's waves in LDS
+//    and across blocks by a small finalize kernel (value, then lowest index).
 #include <math.h>
 
 #include "device_common.h"
@@ -29,114 +30,211 @@ struct Cand {
   int i;
 };
 
-template <int RA, int NB>
-__global__ __launch_bounds__(256) void lmhead_bf16_kernel(const uint16_t* __restrict__ X,
-                                                          const uint16_t* __restrict__ Wt, int N, int H,
-                                                          int V, Cand* __restrict__ partial,
-                                                          float* __restrict__ logits) {
-  constexpr int ROWS = 4 * 32 * RA;  // rows per block
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+#define OOO_LDS(p) ((__attribute__((address_space(3))) void*)(p))
+#define OOO_GLB(p) ((const __attribute__((address_space(1))) void*)(p))
+
+__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x0F70);
+}
+
+constexpr int kLmRows = 128;  // vocabulary rows per tile (4 waves x 32)
+
+// Ring of NS stages; NS - 2 chunks are in flight while one is consumed.
+// Wider node tiles need more X bytes per stage, so fewer stages fit.
+template <int NB>
+struct LmRing {
+  static constexpr int XR = 32 * NB;            // node rows staged (padded)
+  static constexpr int WS = kLmRows * 128;      // bytes of a W chunk
+  static constexpr int XS = XR * 128;           // bytes of an X chunk
+  static constexpr int NS = NB <= 2 ? 5 : NB == 4 ? 4 : 3;
+  static constexpr int XREG = NS * WS;          // start of the X stages
+  static constexpr int BYTES = NS * (WS + XS);
+  static constexpr int WDMA = WS / 1024;        // DMA instructions per W chunk
+  static constexpr int XDMA = XS / 1024;
+  static_assert((NS - 2) * WDMA <= 63 && (NS - 2) * XDMA <= 63, "vmcnt range");
+  static_assert(BYTES + 4 * 32 * NB * 8 <= 160 * 1024, "LDS capacity");
+};
+
+// wait until at most `ahead` chunks of `per` DMA instructions are pending
+template <int PER, int MAXA>
+__device__ __forceinline__ void wait_chunks(int ahead) {
+  if (MAXA >= 3 && ahead >= 3) wait_vmcnt<(MAXA >= 3 ? 3 * PER : 0)>();
+  else if (MAXA >= 2 && ahead == 2) wait_vmcnt<(MAXA >= 2 ? 2 * PER : 0)>();
+  else if (ahead == 1) wait_vmcnt<PER>();
+  else wait_vmcnt<0>();
+}
+
+template <int NB, bool PACKED>
+__global__ __launch_bounds__(384) void lmhead_bf16_kernel(const uint16_t* __restrict__ X,
+                                                          const uint16_t* __restrict__ Wt, int N, int H, int V,
+                                                          Cand* __restrict__ partial, float* __restrict__ logits) {
+  using R = LmRing<NB>;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[R::BYTES];
   __shared__ Cand red[4][32 * NB];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int c = lane & 31, u = lane >> 5;
-  const int v0 = blockIdx.x * ROWS + wave * 32 * RA;
-
-  const uint16_t* wp[RA];
-  const uint16_t* xp[NB];
-#pragma unroll
-  for (int ra = 0; ra < RA; ++ra) {
-    int r = v0 + 32 * ra + c;
-    r = r < V ? r : V - 1;
-    wp[ra] = Wt + (size_t)r * H + 32 * u;
-  }
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    int n = 32 * nb + c;
-    n = n < N ? n : N - 1;
-    xp[nb] = X + (size_t)n * H + 32 * u;
-  }
-
-  f32x16 acc[RA][NB];
-#pragma unroll
-  for (int ra = 0; ra < RA; ++ra)
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) acc[ra][nb] = f32x16{};
-
-  u32x4 wa[RA][4], xa[NB][4], wb[RA][4], xb[NB][4];
-  auto load = [&](u32x4 (&w)[RA][4], u32x4 (&x)[NB][4], int k0) {
-#pragma unroll
-    for (int ra = 0; ra < RA; ++ra)
-#pragma unroll
-      for (int s = 0; s < 4; ++s) w[ra][s] = ld16(wp[ra] + k0 + 8 * s);
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-      for (int s = 0; s < 4; ++s) x[nb][s] = ld16(xp[nb] + k0 + 8 * s);
-  };
-  auto mma = [&](u32x4 (&w)[RA][4], u32x4 (&x)[NB][4]) {
-#pragma unroll
-    for (int s = 0; s < 4; ++s)
-#pragma unroll
-      for (int ra = 0; ra < RA; ++ra)
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) acc[ra][nb] = mfma32(as_bf16x8(w[ra][s]), as_bf16x8(x[nb][s]), acc[ra][nb]);
-  };
-
   const int chunks = H / 64;
-  load(wa, xa, 0);
-  int kc = 0;
-  for (; kc + 2 <= chunks; kc += 2) {
-    load(wb, xb, (kc + 1) * 64);
-    mma(wa, xa);
-    if (kc + 2 < chunks) load(wa, xa, (kc + 2) * 64);
-    mma(wb, xb);
-  }
-  if (kc < chunks) mma(wa, xa);
+  const int ntiles_all = (V + kLmRows - 1) / kLmRows;
+  const int my_tiles = ntiles_all > (int)blockIdx.x ? (ntiles_all - 1 - (int)blockIdx.x) / (int)gridDim.x + 1 : 0;
+  const int total = my_tiles * chunks;  // chunks this block streams
 
-  // acc[ra][nb][j]: vocabulary row v0 + 32ra + 8(j/4) + 4u + j%4, node 32nb + c
+  if (wave >= 4) {
+    // ---------------------------------------------------- loaders: W (4), X (5)
+    const bool is_x = wave == 5;
+    auto issue = [&](int q, int stage) {
+      const int tile = (int)blockIdx.x + (q / chunks) * (int)gridDim.x;
+      const int kc = q % chunks;
+      if (!is_x) {
+        uint8_t* dst = lds + stage * R::WS;
+        if (PACKED) {
+          // the chunk is one contiguous 16 KiB block, already swizzled
+          const uint16_t* src = Wt + ((size_t)tile * chunks + kc) * (kLmRows * 64) + lane * 8;
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    float bv = -INFINITY;
-    int bi = 0x7FFFFFFF;
+          for (int j = 0; j < R::WDMA; ++j)
+            __builtin_amdgcn_global_load_lds(OOO_GLB(src + j * 512), OOO_LDS(dst + j * 1024), 16, 0, 0);
+        } else {
 #pragma unroll
-    for (int ra = 0; ra < RA; ++ra)
+          for (int j = 0; j < R::WDMA; ++j) {
+            const int r = 8 * j + lane / 8;  // tile row; lane = (row, physical piece)
+            const int pc = (lane % 8) ^ (r % 8);
+            const int row = min(tile * kLmRows + r, V - 1);
+            __builtin_amdgcn_global_load_lds(OOO_GLB(Wt + (size_t)row * H + kc * 64 + pc * 8),
+                                             OOO_LDS(dst + j * 1024), 16, 0, 0);
+          }
+        }
+      } else {
+        uint8_t* dst = lds + R::XREG + stage * R::XS;
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int r = v0 + 32 * ra + 8 * (j / 4) + 4 * u + (j % 4);
-        const float val = acc[ra][nb][j];
-        if (r < V && val > bv) {
-          bv = val;
-          bi = r;
+        for (int j = 0; j < R::XDMA; ++j) {
+          const int r = 8 * j + lane / 8;
+          const int pc = (lane % 8) ^ (r % 8);
+          const int row = min(r, N - 1);
+          __builtin_amdgcn_global_load_lds(OOO_GLB(X + (size_t)row * H + kc * 64 + pc * 8),
+                                           OOO_LDS(dst + j * 1024), 16, 0, 0);
         }
       }
-    const float ov = shfl_xor_f(bv, 32);
-    const int oi = shfl_xor_i(bi, 32);
-    if (better(ov, oi, bv, bi)) {
-      bv = ov;
-      bi = oi;
+    };
+    for (int q = 0; q < R::NS - 1 && q < total; ++q) issue(q, q);
+    for (int q = 0; q < total; ++q) {
+      const int ahead = min(R::NS - 2, total - 1 - q);  // chunks issued after q
+      if (is_x) wait_chunks<R::XDMA, R::NS - 2>(ahead);
+      else wait_chunks<R::WDMA, R::NS - 2>(ahead);
+      wg_barrier();
+      if (q + R::NS - 1 < total) issue(q + R::NS - 1, (q + R::NS - 1) % R::NS);
     }
-    if (u == 0) red[wave][32 * nb + c] = Cand{bv, bi};
+    __syncthreads();  // matches the compute waves' final reduction barrier
+    return;
   }
-  if (logits) {
+
+  // ------------------------------------------------------------------ compute
+  const int c = lane & 31, u = lane >> 5;
+  uint32_t off[4];  // piece 2s+u of row c, swizzled
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const int n = 32 * nb + c;
-      if (n < N)
+  for (int s4 = 0; s4 < 4; ++s4) off[s4] = c * 128 + (((2 * s4 + u) ^ (c % 8)) << 4);
+  const uint32_t wrow = wave * 32 * 128;
+
+  float bestv[NB];
+  int besti[NB];
 #pragma unroll
-        for (int ra = 0; ra < RA; ++ra)
+  for (int nb = 0; nb < NB; ++nb) {
+    bestv[nb] = -INFINITY;
+    besti[nb] = 0x7FFFFFFF;
+  }
+  f32x16 acc[NB];
+  for (int q = 0; q < total; ++q) {
+    const int kc = q % chunks;
+    if (kc == 0) {
 #pragma unroll
-          for (int j = 0; j < 16; ++j) {
-            const int r = v0 + 32 * ra + 8 * (j / 4) + 4 * u + (j % 4);
-            if (r < V) logits[(size_t)n * V + r] = acc[ra][nb][j];
+      for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x16{};
+    }
+    const int stage = q % R::NS;
+    wg_barrier();
+    const uint8_t* Ws = lds + stage * R::WS + wrow;
+    const uint8_t* Xs = lds + R::XREG + stage * R::XS;
+    bf16x8 af[4], bf[NB][4];
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4) {
+      af[s4] = as_bf16x8(*reinterpret_cast<const u32x4*>(Ws + off[s4]));
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) bf[nb][s4] = as_bf16x8(*reinterpret_cast<const u32x4*>(Xs + nb * 4096 + off[s4]));
+    }
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) acc[nb] = mfma32(af[s4], bf[nb][s4], acc[nb]);
+
+    if (kc == chunks - 1) {
+      // tile done: acc[nb][j] = logit of vocabulary row v0 + 8(j/4) + 4u + j%4, node 32nb + c
+      const int tile = (int)blockIdx.x + (q / chunks) * (int)gridDim.x;
+      const int v0 = tile * kLmRows + wave * 32;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        float bv = -INFINITY;
+        int bi = 0x7FFFFFFF;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const int r = v0 + 8 * (j / 4) + 4 * u + (j % 4);
+          if (r < V && acc[nb][j] > bv) {
+            bv = acc[nb][j];
+            bi = r;
           }
+        }
+        const float ov = shfl_xor_f(bv, 32);
+        const int oi = shfl_xor_i(bi, 32);
+        if (better(ov, oi, bv, bi)) {
+          bv = ov;
+          bi = oi;
+        }
+        if (better(bv, bi, bestv[nb], besti[nb])) {
+          bestv[nb] = bv;
+          besti[nb] = bi;
+        }
+        if (logits) {
+          const int n = 32 * nb + c;
+          if (n < N)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+              const int r = v0 + 8 * (j / 4) + 4 * u + (j % 4);
+              if (r < V) logits[(size_t)n * V + r] = acc[nb][j];
+            }
+        }
+      }
     }
   }
+  if (u == 0)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) red[wave][32 * nb + c] = Cand{bestv[nb], besti[nb]};
   __syncthreads();
-  for (int n = threadIdx.x; n < N && n < 32 * NB; n += blockDim.x) {
+  for (int n = threadIdx.x; n < N; n += 256) {
     Cand b = red[0][n];
-    for (int w = 1; w < 4; ++w)
-      if (better(red[w][n].v, red[w][n].i, b.v, b.i)) b = red[w][n];
+    for (int w2 = 1; w2 < 4; ++w2)
+      if (better(red[w2][n].v, red[w2][n].i, b.v, b.i)) b = red[w2][n];
     partial[(size_t)blockIdx.x * N + n] = b;
   }
+}
+
+// Packed weight layout: for tile t (128 rows) and chunk kc (64 columns), the
+// 16 KiB block at ((t * chunks + kc) * 128 + r) * 64 elements holds row
+// t*128 + r; its physical 16-byte piece p holds columns kc*64 + 8*(p ^ r%8)
+// .. +8, the swizzle the kernel's LDS reads expect.  Rows >= V are zero.
+__global__ __launch_bounds__(256) void lmhead_pack_kernel(const uint16_t* __restrict__ W, int V, int H,
+                                                          uint16_t* __restrict__ out, long long pieces) {
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= pieces) return;
+  const int chunks = H / 64;
+  const int p = (int)(i % 8);
+  const int r = (int)((i / 8) % kLmRows);
+  const long long tk = i / (8 * kLmRows);  // t * chunks + kc
+  const int kc = (int)(tk % chunks);
+  const long long t = tk / chunks;
+  const long long row = t * kLmRows + r;
+  u32x4 v = {0, 0, 0, 0};
+  if (row < V) v = ld16(W + row * H + kc * 64 + ((p ^ (r % 8)) * 8));
+  st16(out + i * 8, v);
 }
 
 // float32 path: one thread per vocabulary row, one block column per node.
@@ -193,31 +291,32 @@ __global__ __launch_bounds__(256) void lmhead_finalize_kernel(const Cand* __rest
 }
 
 struct LmPlan {
-  int ra, nb, rows, blocks;
+  int nb, blocks;
   size_t ws_bytes;
 };
+
+// Blocks of the persistent bf16 grid: one per compute unit of the device.
+int device_cus() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
 
 LmPlan lm_plan(int N, int H, int V, ooo_dtype dt) {
   LmPlan p{};
   if (dt == OOO_BF16) {
-    if (N <= 32) {
-      p.ra = 4;
-      p.nb = 1;
-    } else if (N <= 64) {
-      p.ra = 2;
-      p.nb = 2;
-    } else if (N <= 128) {
-      p.ra = 2;
-      p.nb = 4;
-    } else {
-      p.ra = 1;
-      p.nb = 8;
-    }
-    p.rows = 128 * p.ra;
+    p.nb = N <= 32 ? 1 : N <= 64 ? 2 : N <= 128 ? 4 : 8;
+    const int tiles = (V + kLmRows - 1) / kLmRows;
+    p.blocks = tiles < device_cus() ? tiles : device_cus();
   } else {
-    p.rows = 256;
+    p.blocks = (V + 255) / 256;
   }
-  p.blocks = (V + p.rows - 1) / p.rows;
   p.ws_bytes = (size_t)p.blocks * N * sizeof(Cand);
   return p;
 }
@@ -232,20 +331,46 @@ extern "C" size_t ooo_lmhead_workspace(int32_t n_nodes, int32_t hidden_dim, int3
   return lm_plan(n_nodes, hidden_dim, vocab, dt).ws_bytes;
 }
 
+extern "C" size_t ooo_lmhead_packed_bytes(int32_t vocab, int32_t hidden_dim, ooo_dtype dt) {
+  if (vocab < 1 || hidden_dim < 1 || hidden_dim % 64 || dt != OOO_BF16) return 0;
+  const size_t tiles = (vocab + kLmRows - 1) / kLmRows;
+  return tiles * kLmRows * (size_t)hidden_dim * 2;
+}
+
+extern "C" int ooo_lmhead_pack(const void* weight, int32_t vocab, int32_t hidden_dim, ooo_dtype dt, void* packed,
+                               size_t packed_bytes, void* stream) {
+  OOO_REQUIRE(weight && packed, OOO_ERR_INVALID, "ooo_lmhead_pack: null pointer");
+  OOO_REQUIRE(vocab >= 1 && hidden_dim >= 1, OOO_ERR_INVALID, "ooo_lmhead_pack: sizes must be positive");
+  OOO_REQUIRE(dt == OOO_BF16, OOO_ERR_UNSUPPORTED, "ooo_lmhead_pack: only OOO_BF16 weights are packed");
+  OOO_REQUIRE(hidden_dim % 64 == 0, OOO_ERR_UNSUPPORTED, "ooo_lmhead_pack: hidden_dim %% 64 != 0");
+  const size_t need = ooo_lmhead_packed_bytes(vocab, hidden_dim, dt);
+  OOO_REQUIRE(packed_bytes >= need, OOO_ERR_CAPACITY, "ooo_lmhead_pack: %zu bytes needed (got %zu)", need,
+              packed_bytes);
+  const long long pieces = (long long)(need / 16);
+  lmhead_pack_kernel<<<(unsigned)((pieces + 255) / 256), 256, 0, reinterpret_cast<hipStream_t>(stream)>>>(
+      (const uint16_t*)weight, vocab, hidden_dim, (uint16_t*)packed, pieces);
+  const hipError_t e = hipGetLastError();
+  OOO_REQUIRE(e == hipSuccess, OOO_ERR_HIP, "ooo_lmhead_pack: launch failed: %s", hipGetErrorString(e));
+  return ooo::ok();
+}
+
 extern "C" int ooo_lmhead_argmax(const void* hidden, const void* weight, int32_t n_nodes, int32_t hidden_dim,
-                                 int32_t vocab, ooo_dtype dt, int32_t* argmax_ids, float* max_logit,
-                                 float* logits, void* workspace, size_t ws_bytes, void* stream) {
+                                 int32_t vocab, ooo_dtype dt, int32_t weight_layout, int32_t* argmax_ids,
+                                 float* max_logit, float* logits, void* workspace, size_t ws_bytes, void* stream) {
   OOO_REQUIRE(hidden && weight && argmax_ids && max_logit, OOO_ERR_INVALID, "ooo_lmhead_argmax: null pointer");
   OOO_REQUIRE(n_nodes >= 1 && hidden_dim >= 1 && vocab >= 1, OOO_ERR_INVALID,
               "ooo_lmhead_argmax: sizes must be positive (n_nodes=%d hidden_dim=%d vocab=%d)", n_nodes,
               hidden_dim, vocab);
   OOO_REQUIRE(dt == OOO_F32 || dt == OOO_BF16, OOO_ERR_INVALID, "ooo_lmhead_argmax: unknown dtype %d", (int)dt);
+  OOO_REQUIRE(weight_layout == OOO_W_ROWS || weight_layout == OOO_W_PACKED, OOO_ERR_INVALID,
+              "ooo_lmhead_argmax: unknown weight layout %d", weight_layout);
   if (dt == OOO_BF16) {
     OOO_REQUIRE(hidden_dim % 64 == 0, OOO_ERR_UNSUPPORTED, "ooo_lmhead_argmax: bf16 needs hidden_dim %% 64 == 0");
     OOO_REQUIRE(n_nodes <= 256, OOO_ERR_UNSUPPORTED, "ooo_lmhead_argmax: bf16 supports up to 256 nodes");
   } else {
     OOO_REQUIRE(hidden_dim % 4 == 0, OOO_ERR_UNSUPPORTED, "ooo_lmhead_argmax: f32 needs hidden_dim %% 4 == 0");
     OOO_REQUIRE(n_nodes <= 65535, OOO_ERR_UNSUPPORTED, "ooo_lmhead_argmax: too many nodes");
+    OOO_REQUIRE(weight_layout == OOO_W_ROWS, OOO_ERR_UNSUPPORTED, "ooo_lmhead_argmax: f32 weights are row-major only");
   }
   const LmPlan p = lm_plan(n_nodes, hidden_dim, vocab, dt);
   OOO_REQUIRE(workspace && ws_bytes >= p.ws_bytes, OOO_ERR_CAPACITY,
@@ -255,14 +380,19 @@ extern "C" int ooo_lmhead_argmax(const void* hidden, const void* weight, int32_t
   if (dt == OOO_BF16) {
     const uint16_t* X = (const uint16_t*)hidden;
     const uint16_t* W = (const uint16_t*)weight;
-    if (p.nb == 1)
-      lmhead_bf16_kernel<4, 1><<<p.blocks, 256, 0, st>>>(X, W, n_nodes, hidden_dim, vocab, part, logits);
-    else if (p.nb == 2)
-      lmhead_bf16_kernel<2, 2><<<p.blocks, 256, 0, st>>>(X, W, n_nodes, hidden_dim, vocab, part, logits);
-    else if (p.nb == 4)
-      lmhead_bf16_kernel<2, 4><<<p.blocks, 256, 0, st>>>(X, W, n_nodes, hidden_dim, vocab, part, logits);
-    else
-      lmhead_bf16_kernel<1, 8><<<p.blocks, 256, 0, st>>>(X, W, n_nodes, hidden_dim, vocab, part, logits);
+    const bool pk = weight_layout == OOO_W_PACKED;
+#define OOO_LM_LAUNCH(NBV)                                                                                   \
+  do {                                                                                                      \
+    if (pk)                                                                                                 \
+      lmhead_bf16_kernel<NBV, true><<<p.blocks, 384, 0, st>>>(X, W, n_nodes, hidden_dim, vocab, part, logits); \
+    else                                                                                                    \
+      lmhead_bf16_kernel<NBV, false><<<p.blocks, 384, 0, st>>>(X, W, n_nodes, hidden_dim, vocab, part, logits); \
+  } while (0)
+    if (p.nb == 1) OOO_LM_LAUNCH(1);
+    else if (p.nb == 2) OOO_LM_LAUNCH(2);
+    else if (p.nb == 4) OOO_LM_LAUNCH(4);
+    else OOO_LM_LAUNCH(8);
+#undef OOO_LM_LAUNCH
   } else {
     lmhead_f32_kernel<<<dim3(p.blocks, n_nodes), 256, 0, st>>>((const float*)hidden, (const float*)weight, n_nodes,
                                                               hidden_dim, vocab, part, logits);

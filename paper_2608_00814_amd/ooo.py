@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libooo.so")
 
 OK, ERR_INVALID, ERR_UNSUPPORTED, ERR_CAPACITY, ERR_HIP = 0, -1, -2, -3, -4
 F32, BF16 = 0, 1
+W_ROWS, W_PACKED = 0, 1  # ooo_weight_layout
 
 _c_i32p = ctypes.POINTER(ctypes.c_int32)
 _c_u64p = ctypes.POINTER(ctypes.c_uint64)
@@ -37,7 +38,10 @@ SIGNATURES = {
     "ooo_tree_attn": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _i32, _vp, _i32, _i32, _i32, _i32,
                                      ctypes.c_float, ctypes.c_int, _vp, _vp, _sz, _vp]),
     "ooo_lmhead_workspace": (_sz, [_i32, _i32, _i32, ctypes.c_int]),
-    "ooo_lmhead_argmax": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, ctypes.c_int, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "ooo_lmhead_packed_bytes": (_sz, [_i32, _i32, ctypes.c_int]),
+    "ooo_lmhead_pack": (ctypes.c_int, [_vp, _i32, _i32, ctypes.c_int, _vp, _sz, _vp]),
+    "ooo_lmhead_argmax": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, ctypes.c_int, _i32, _vp, _vp, _vp, _vp, _sz,
+                                         _vp]),
     "ooo_accept": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i32, _vp, _i32, _i32, _vp, _vp, _vp, _vp]),
     "ooo_kv_compact": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i64, _i32, ctypes.c_int, _i32, _i32, _vp, _vp,
                                       _i32, _vp]),
@@ -166,19 +170,48 @@ def lmhead_workspace(n_nodes: int, hidden_dim: int, vocab: int, dtype: int) -> i
     return int(lib().ooo_lmhead_workspace(n_nodes, hidden_dim, vocab, dtype))
 
 
+class PackedWeight:
+    """LM-head weight in the streaming layout of ooo_lmhead_pack: a flat
+    uint8 device tensor plus the logical [vocab][hidden_dim] shape."""
+
+    def __init__(self, data, vocab: int, hidden_dim: int, dtype: int):
+        self.data, self.vocab, self.hidden_dim, self.dtype = data, vocab, hidden_dim, dtype
+
+
+def lmhead_pack(weight, stream=None) -> PackedWeight:
+    """Packs a [V][H] bf16 device weight (allocates the packed copy)."""
+    import torch
+    _dev(weight, "weight")
+    V, H = weight.shape
+    code = dtype_code(weight)
+    need = int(lib().ooo_lmhead_packed_bytes(V, H, code))
+    if need == 0:
+        raise OooError(ERR_UNSUPPORTED, f"no packed layout for {tuple(weight.shape)} {weight.dtype}")
+    data = torch.empty(need, dtype=torch.uint8, device=weight.device)
+    _check(lib().ooo_lmhead_pack(weight.data_ptr(), V, H, code, data.data_ptr(), need, _stream(stream)))
+    return PackedWeight(data, V, H, code)
+
+
 def lmhead_argmax(hidden, weight, argmax_ids, max_logit, logits=None, workspace=None, stream=None) -> None:
-    """hidden [N][H]; weight [V][H]; argmax_ids int32 [N]; max_logit float32
-    [N]; logits optional float32 [N][V]."""
-    for t, nm in ((hidden, "hidden"), (weight, "weight"), (argmax_ids, "argmax_ids"), (max_logit, "max_logit")):
+    """hidden [N][H]; weight [V][H] device tensor or a PackedWeight;
+    argmax_ids int32 [N]; max_logit float32 [N]; logits optional float32 [N][V]."""
+    packed = isinstance(weight, PackedWeight)
+    wt = weight.data if packed else weight
+    for t, nm in ((hidden, "hidden"), (wt, "weight"), (argmax_ids, "argmax_ids"), (max_logit, "max_logit")):
         _dev(t, nm)
     if logits is not None:
         _dev(logits, "logits")
     N, H = hidden.shape
-    V = weight.shape[0]
+    if packed:
+        if weight.hidden_dim != H or weight.dtype != dtype_code(hidden):
+            raise OooError(ERR_INVALID, "packed weight does not match the hidden rows")
+        V = weight.vocab
+    else:
+        V = weight.shape[0]
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    _check(lib().ooo_lmhead_argmax(hidden.data_ptr(), weight.data_ptr(), N, H, V, dtype_code(hidden),
-                                   argmax_ids.data_ptr(), max_logit.data_ptr(), _ptr(logits), _ptr(workspace),
-                                   ws_bytes, _stream(stream)))
+    _check(lib().ooo_lmhead_argmax(hidden.data_ptr(), wt.data_ptr(), N, H, V, dtype_code(hidden),
+                                   W_PACKED if packed else W_ROWS, argmax_ids.data_ptr(), max_logit.data_ptr(),
+                                   _ptr(logits), _ptr(workspace), ws_bytes, _stream(stream)))
 
 
 def accept(token, parent, depth, anc_mask, argmax_ids, n_nodes: int, path, accept_len, bonus_token,

@@ -127,8 +127,13 @@ class VerifyRunner:
         return StepResult(self.n_nodes, int(self.packed["n_truncated"]) if self.packed else 0, L, int(r[1]),
                           r[2:2 + L + 1].copy())
 
-    def set_weight(self, weight) -> None:
-        self._weight = weight
+    def set_weight(self, weight, packed: Optional[bool] = None) -> None:
+        """Binds the LM-head weight [V][H].  bf16 weights are re-laid out once
+        for streaming (ooo_lmhead_pack) unless packed=False; the row-major
+        tensor is then no longer referenced."""
+        if packed is None:
+            packed = self.code == ooo.BF16 and weight.shape[1] % 64 == 0
+        self._weight = ooo.lmhead_pack(weight) if packed else weight
 
     def device_step(self, q_layers: Sequence, k_cache, v_cache, hidden, prefix_len: int,
                     logits=None, compact: bool = True) -> None:

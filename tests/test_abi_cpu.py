@@ -27,7 +27,7 @@ def declared_functions():
 
 def test_exports_match_header():
     names = declared_functions()
-    assert len(names) == 9
+    assert len(names) == 11
     assert set(names) == set(ooo.SIGNATURES)
     lib = ooo.lib()
     for n in names:
@@ -126,7 +126,7 @@ def test_device_entry_points_validate_on_host():
     assert L.ooo_tree_attn(None, fake, fake, 100, 10, 4, fake, 1, 4, 1, 64, 0.1, ooo.BF16, fake, None, 0, None) \
         == ooo.ERR_INVALID
     assert "null" in ooo.last_error()
-    assert L.ooo_lmhead_argmax(fake, None, 4, 64, 100, ooo.BF16, fake, fake, None, fake, 1 << 20, None) \
+    assert L.ooo_lmhead_argmax(fake, None, 4, 64, 100, ooo.BF16, ooo.W_ROWS, fake, fake, None, fake, 1 << 20, None) \
         == ooo.ERR_INVALID
     assert L.ooo_accept(fake, fake, fake, fake, 1, fake, 4, 8, None, fake, fake, None) == ooo.ERR_INVALID
     assert L.ooo_kv_compact(fake, fake, 2, 2, 100, 64, ooo.BF16, 10, 4, None, fake, 8, None) == ooo.ERR_INVALID
@@ -145,15 +145,27 @@ def test_device_entry_points_validate_on_host():
     # unsupported but valid
     assert L.ooo_tree_attn(fake, fake, fake, 100, 10, 4, fake, 1, 4, 1, 96, 0.1, ooo.BF16, fake, None, 0, None) \
         == ooo.ERR_UNSUPPORTED
-    assert L.ooo_lmhead_argmax(fake, fake, 4, 100, 1000, ooo.BF16, fake, fake, None, fake, 1 << 20, None) \
+    assert L.ooo_lmhead_argmax(fake, fake, 4, 100, 1000, ooo.BF16, ooo.W_ROWS, fake, fake, None, fake, 1 << 20, None) \
         == ooo.ERR_UNSUPPORTED
-    assert L.ooo_lmhead_argmax(fake, fake, 300, 128, 1000, ooo.BF16, fake, fake, None, fake, 1 << 20, None) \
+    assert L.ooo_lmhead_argmax(fake, fake, 300, 128, 1000, ooo.BF16, ooo.W_ROWS, fake, fake, None, fake, 1 << 20, None) \
         == ooo.ERR_UNSUPPORTED
     assert L.ooo_kv_compact(fake, fake, 2, 2, 100, 4, ooo.BF16, 10, 4, fake, fake, 8, None) == ooo.ERR_UNSUPPORTED
+    # weight layouts
+    assert L.ooo_lmhead_argmax(fake, fake, 4, 64, 1000, ooo.BF16, 2, fake, fake, None, fake, 1 << 20, None) \
+        == ooo.ERR_INVALID
+    assert L.ooo_lmhead_argmax(fake, fake, 4, 64, 1000, ooo.F32, ooo.W_PACKED, fake, fake, None, fake, 1 << 20,
+                               None) == ooo.ERR_UNSUPPORTED
+    assert L.ooo_lmhead_packed_bytes(1000, 64, ooo.BF16) == 8 * 128 * 64 * 2  # 8 tiles of 128 rows
+    assert L.ooo_lmhead_packed_bytes(1000, 100, ooo.BF16) == 0
+    assert L.ooo_lmhead_packed_bytes(1000, 64, ooo.F32) == 0
+    assert L.ooo_lmhead_pack(fake, 1000, 64, ooo.BF16, None, 1 << 20, None) == ooo.ERR_INVALID
+    assert L.ooo_lmhead_pack(fake, 1000, 64, ooo.F32, fake, 1 << 20, None) == ooo.ERR_UNSUPPORTED
+    assert L.ooo_lmhead_pack(fake, 1000, 100, ooo.BF16, fake, 1 << 20, None) == ooo.ERR_UNSUPPORTED
+    assert L.ooo_lmhead_pack(fake, 1000, 64, ooo.BF16, fake, 8 * 128 * 64 * 2 - 1, None) == ooo.ERR_CAPACITY
     # workspace too small
     need = L.ooo_lmhead_workspace(4, 64, 1000, ooo.BF16)
     assert need > 0
-    assert L.ooo_lmhead_argmax(fake, fake, 4, 64, 1000, ooo.BF16, fake, fake, None, fake, need - 1, None) \
+    assert L.ooo_lmhead_argmax(fake, fake, 4, 64, 1000, ooo.BF16, ooo.W_ROWS, fake, fake, None, fake, need - 1, None) \
         == ooo.ERR_CAPACITY
     need = L.ooo_tree_attn_workspace(64, 32, 8, 128, 4096, ooo.BF16)
     assert need > 0

@@ -195,11 +195,13 @@ LM_CASES = [
 ]
 
 
-def _run_lm(x, w, dt, want_logits=True):
+def _run_lm(x, w, dt, want_logits=True, packed=False):
     N, H = x.shape
     V = w.shape[0]
     code = ooo.BF16 if dt == "bf16" else ooo.F32
     xd, wd = gh.to_dev(x, dt, DEV), gh.to_dev(w, dt, DEV)
+    if packed:
+        wd = ooo.lmhead_pack(wd)
     ids = torch.full((N,), -7, dtype=torch.int32, device=DEV)
     mx = torch.empty(N, dtype=torch.float32, device=DEV)
     lg = torch.empty(N, V, dtype=torch.float32, device=DEV) if want_logits else None
@@ -209,15 +211,19 @@ def _run_lm(x, w, dt, want_logits=True):
     return ids.cpu().numpy(), mx.cpu().numpy(), (lg.cpu().numpy() if want_logits else None)
 
 
-@pytest.mark.parametrize("case", LM_CASES, ids=[f"N{c[0]}-H{c[1]}-V{c[2]}-{c[3]}" for c in LM_CASES])
-def test_lmhead_edges(case):
+LM_RUNS = [(c, False) for c in LM_CASES] + [(c, True) for c in LM_CASES if c[3] == "bf16"]
+
+
+@pytest.mark.parametrize("case,packed", LM_RUNS,
+                         ids=[f"N{c[0]}-H{c[1]}-V{c[2]}-{c[3]}{'-packed' if p else ''}" for c, p in LM_RUNS])
+def test_lmhead_edges(case, packed):
     N, H, V, dt = case
-    print(f"case lmhead {case}", flush=True)
+    print(f"case lmhead {case} packed={packed}", flush=True)
     rs = np.random.default_rng(N * 7 + H + V)
     x = _store(rs.normal(size=(N, H)), dt)
     # logit spread of about one unit so most nodes clear the tie-exclusion margin
     w = _store(rs.normal(size=(V, H)) * max(0.02, 1.0 / math.sqrt(H)), dt)
-    ids, mx, lg = _run_lm(x, w, dt)
+    ids, mx, lg = _run_lm(x, w, dt, packed=packed)
     ref = ov.lm_head_logits(wl.to_f64(x, dt), wl.to_f64(w, dt))
     g = ov.greedy_tokens(ref)
     tol = gh.LOGIT_TOL if dt == "bf16" else 1e-5
@@ -228,10 +234,11 @@ def test_lmhead_edges(case):
     assert np.allclose(mx[clear], g["max_logit"][clear], rtol=1e-3, atol=1e-3)
 
 
-def test_lmhead_exact_ties_go_to_lowest_index():
+@pytest.mark.parametrize("packed", [False, True])
+def test_lmhead_exact_ties_go_to_lowest_index(packed):
     """Identical weight rows in different blocks give identical logits; the
     lowest vocabulary index must win for every node."""
-    print("case lmhead ties", flush=True)
+    print(f"case lmhead ties packed={packed}", flush=True)
     N, H, V = 64, 256, 70001
     rs = np.random.default_rng(5)
     x = _bf16(rs.normal(size=(N, H)))
@@ -242,10 +249,33 @@ def test_lmhead_exact_ties_go_to_lowest_index():
         a, b, c = sorted(rs.choice(V, size=3, replace=False).tolist())
         row = _bf16(xf[n] * 0.05)
         w[a] = w[b] = w[c] = row
-    ids, mx, _ = _run_lm(x, w, "bf16", want_logits=False)
+    ids, mx, _ = _run_lm(x, w, "bf16", want_logits=False, packed=packed)
     ref = ov.greedy_tokens(ov.lm_head_logits(xf, wl.to_f64(w, "bf16")))
     # the reference breaks exact ties to the lowest index too
     assert np.array_equal(ids, ref["ids"])
+
+
+@pytest.mark.parametrize("V,H", [(1000, 64), (128, 128), (300, 192)])
+def test_lmhead_pack_layout(V, H):
+    """The packed weight is a pure re-layout: tile t, chunk kc, row r and
+    physical 16-byte piece p hold columns kc*64 + 8*(p ^ r%8) .. +8 of row
+    t*128 + r, and rows past the vocabulary are zero."""
+    print(f"case lmhead pack V={V} H={H}", flush=True)
+    rs = np.random.default_rng(V + H)
+    w = _bf16(rs.normal(size=(V, H)))
+    pw = ooo.lmhead_pack(gh.to_dev(w, "bf16", DEV))
+    torch.cuda.synchronize()
+    got = pw.data.cpu().numpy().view(np.uint16)
+    T, C = (V + 127) // 128, H // 64
+    full = np.zeros((T * 128, H), np.uint16)
+    full[:V] = w  # bf16 bit patterns
+    want = np.empty((T, C, 128, 8, 8), np.uint16)
+    for r in range(128):
+        for p in range(8):
+            q = p ^ (r % 8)
+            for kc in range(C):
+                want[:, kc, r, p, :] = full[r::128][:T, kc * 64 + 8 * q:kc * 64 + 8 * q + 8]
+    assert np.array_equal(got, want.reshape(-1))
 
 
 # ----------------------------------------------------------------------------
