@@ -9,22 +9,30 @@ committed prefix rows, 64-node trie, hidden 4096, vocabulary 151936, bf16):
   host   ooo_pack_tree of the step's candidates (hint, FSM chain, 2 retrieved)
   graph  H2D of the packed trie; the node K/V rows written into cache rows
          [P, P+N) of every layer (the model's projection output, staged from
-         a resident copy); 36 x ooo_tree_attn
+         a resident copy)
+  graph  36 x ooo_tree_attn, bracketed by HIP events on its stream
   eager  ooo_lmhead_argmax, bracketed by HIP events on its stream
   graph  ooo_accept, ooo_kv_compact, D2H of (L, bonus, path)
   host   stream synchronise and read the accepted length (the next step's
          candidates depend on it in a real decode loop)
 
 All inputs are resident in HBM before timing starts.  Prints one JSON line.
+The roofline object covers ooo_tree_attn, the kernel pair that takes most of
+a step; the LM head has one of its own.  --calibrate-copy-mib M adds one
+plain device copy of M MiB after setup, outside the timed steps, so that
+hardware byte counters read under a profiler can be scaled by what they
+report for a copy of known size.
 """
 
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import math
 import os
 import platform
+import re
 import sys
 import time
 
@@ -49,6 +57,27 @@ def lmhead_bytes(cfg, N):
     """W + X + greedy ids and max logits."""
     e = cfg.elt_bytes
     return cfg.vocab * cfg.hidden * e + N * cfg.hidden * e + N * 8
+
+
+def _source_digest(path: str) -> str:
+    """sha256 prefix of a source file with comments and whitespace removed."""
+    text = open(os.path.join(ROOT, path)).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    return hashlib.sha256(" ".join(text.split()).encode()).hexdigest()[:16]
+
+
+def recorded_traffic(workload: str, entry: str):
+    """HBM bytes per launch that the committed counter profile records for
+    ``entry``, or None when there is none for this workload or the kernel
+    sources have changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path)).get(entry)
+    if not rec or any(_source_digest(f) != d for f, d in rec["sources"].items()):
+        return None
+    return int(rec["bytes_per_launch"])
 
 
 def cpu_baseline(cfg, seconds: float):
@@ -103,6 +132,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="launch every kernel eagerly")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="one plain copy of this many MiB after setup (byte-counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for {args.gpus}); the path runs on a single MI355X.",
@@ -166,13 +197,24 @@ def main():
     torch.cuda.synchronize()
     setup_s = time.time() - t_setup
 
+    if args.calibrate_copy_mib > 0:
+        n = args.calibrate_copy_mib << 18  # float32 elements
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.add(src, 1.0, out=dst)  # reads and writes calibrate_copy_mib MiB each
+        torch.cuda.synchronize()
+        del src, dst
+
     stream = torch.cuda.Stream()  # default priority
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
 
-    def stage_and_attend():
+    def stage():
         runner.upload_tree()
         k_cache[:, :, P:P + N].copy_(k_nodes)
         v_cache[:, :, P:P + N].copy_(v_nodes)
+
+    def attend():
         for l in range(cfg.n_layers):
             runner.attention(l, q_layers[l], k_cache[l], v_cache[l], P)
 
@@ -187,16 +229,19 @@ def main():
         hidden.copy_(hid[0])
         if not args.no_graph:
             # eager warm-up of every kernel before capture
-            stage_and_attend()
+            stage()
+            attend()
             runner.lm_head(hidden)
             tail()
             stream.synchronize()
-            ga, gt = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+            gs, ga, gt = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gs, stream=stream):
+                stage()
             with torch.cuda.graph(ga, stream=stream):
-                stage_and_attend()
+                attend()
             with torch.cuda.graph(gt, stream=stream):
                 tail()
-            graphs = (ga, gt)
+            graphs = (gs, ga, gt)
         stream.synchronize()
 
         lm_ms, attn_ms, Ls = [], [], []
@@ -205,16 +250,20 @@ def main():
             v = i % n_variants
             runner.pack(cand_sets[v].root_token, *csr[v])
             hidden.copy_(hid[v])
-            ev[0].record(stream)
             if graphs:
                 graphs[0].replay()
             else:
-                stage_and_attend()
+                stage()
+            ev[0].record(stream)
+            if graphs:
+                graphs[1].replay()
+            else:
+                attend()
             ev[1].record(stream)
             runner.lm_head(hidden)
             ev[2].record(stream)
             if graphs:
-                graphs[1].replay()
+                graphs[2].replay()
             else:
                 tail()
             stream.synchronize()
@@ -238,12 +287,13 @@ def main():
     steps_per_s = args.steps / elapsed
     tokens_per_s = float(np.sum(np.array(Ls) + 1)) / elapsed
     lm_us = 1e3 * float(np.mean(lm_ms))
-    attn_stage_us = 1e3 * float(np.mean(attn_ms))
-    stage_bytes = 2 * 2 * cfg.n_layers * cfg.n_kv_heads * N * cfg.head_dim * cfg.elt_bytes  # read+write K,V nodes
+    attn_us = 1e3 * float(np.mean(attn_ms))
+    attn_call_us = attn_us / cfg.n_layers
     a_bytes = attention_bytes(cfg, N)
+    a_gbs = a_bytes / (attn_call_us * 1e-6) / 1e9
     lm_b = lmhead_bytes(cfg, N)
     lm_gbs = lm_b / (lm_us * 1e-6) / 1e9
-    path_gbs = (cfg.n_layers * a_bytes + lm_b) / ((attn_stage_us + lm_us) * 1e-6) / 1e9
+    path_gbs = (cfg.n_layers * a_bytes + lm_b) / ((attn_us + lm_us) * 1e-6) / 1e9
 
     out = {
         "metric": METRIC,
@@ -264,16 +314,22 @@ def main():
                    "launch": "eager" if args.no_graph else "hip-graph per phase, LM head eager"},
         "tokens_per_s": round(tokens_per_s, 1),
         "mean_accepted_plus_bonus": round(float(np.mean(np.array(Ls) + 1)), 3),
+        "attention_us_per_step": round(attn_us, 2),
+        "attention_us_per_layer": round(attn_call_us, 3),
         "lmhead_us": round(lm_us, 2),
-        "attention_us_per_step": round(attn_stage_us, 2),
-        "attention_us_per_layer": round(attn_stage_us / cfg.n_layers, 3),
         "path_hbm_gbs": round(path_gbs, 1),
         "path_hbm_frac": round(path_gbs / HBM_PEAK_GBS, 4),
-        "roofline": {"bound": "hbm", "kernel": "lmhead_bf16_kernel (+ finalize)", "achieved": round(lm_gbs, 1),
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(lm_gbs / HBM_PEAK_GBS, 4),
-                     "traffic": None, "bytes_per_launch": lm_b},
+        "roofline": {"bound": "hbm", "kernel": "ooo_tree_attn (tree_attn_bf16_kernel + tree_attn_combine_kernel)",
+                     "achieved": round(a_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(a_gbs / HBM_PEAK_GBS, 4), "traffic": recorded_traffic(cfg.name, "ooo_tree_attn"),
+                     "bytes_per_launch": a_bytes,
+                     "us_per_launch": round(attn_call_us, 3)},
+        "roofline_lmhead": {"bound": "hbm", "kernel": "ooo_lmhead_argmax (lmhead_bf16_kernel + lmhead_finalize_kernel)",
+                            "achieved": round(lm_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                            "frac": round(lm_gbs / HBM_PEAK_GBS, 4),
+                            "traffic": recorded_traffic(cfg.name, "ooo_lmhead_argmax"), "bytes_per_launch": lm_b,
+                            "us_per_launch": round(lm_us, 2)},
         "setup_s": round(setup_s, 1),
-        "notes": f"attention_us_per_step includes the trie H2D and the node K/V staging ({stage_bytes} bytes)",
     }
     if not args.no_cpu_baseline:
         del k_cache, v_cache

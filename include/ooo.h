@@ -3,7 +3,7 @@
  *
  * One verification step of greedy speculative decoding at batch one, as the
  * OoO-Spec paper describes it (Section 3, "Target authority" with Eq. 1 and
- * "The ToolSpec decoding loop"; Section 4.4, "Verify and commit"):
+ * "The ToolSpec decoding loop"; Section 4.5, "Verify and commit"):
  *
  *   ooo_pack_tree      merge priority-ordered draft continuations into a trie
  *   ooo_tree_attn      per layer: every trie node attends to the committed
@@ -62,8 +62,8 @@ int ooo_version(void);
 
 /*
  * ooo_pack_tree - candidate trie (Section 3, ToolSpec loop: candidates are
- * combined into one tree; Section 4.3: Merge_B keeps a fixed candidate
- * budget and hint lanes come first; Section 4.4: hint and native
+ * combined into one tree; Section 4.4: Merge_B keeps a fixed candidate
+ * budget and hint lanes come first; Section 4.5: hint and native
  * continuations are compiled into the same tree).
  *
  * HOST memory only, synchronous.
@@ -92,7 +92,7 @@ int ooo_pack_tree(int32_t root_token, const int32_t* cand_tokens, const int32_t*
                   int32_t* n_nodes, int32_t* n_truncated);
 
 /*
- * ooo_tree_attn - one layer of tree-masked attention (Section 4.4: the target
+ * ooo_tree_attn - one layer of tree-masked attention (Section 4.5: the target
  * scores the whole candidate tree in one forward pass; each node sees what
  * sequential greedy decoding of its own path would see).
  *
@@ -172,7 +172,7 @@ int ooo_lmhead_argmax(const void* hidden, const void* weight, int32_t n_nodes,
                       size_t ws_bytes, void* stream);
 
 /*
- * ooo_accept - longest greedy-agreeing root path (Section 4.4, Verify and
+ * ooo_accept - longest greedy-agreeing root path (Section 4.5, Verify and
  * commit: draft tokens are kept while they equal the target's greedy token
  * at their parent; at the first disagreement the rest is rejected and the
  * target's own token is used).
@@ -197,7 +197,7 @@ int ooo_accept(const int32_t* token, const int32_t* parent, const int32_t* depth
                int32_t* bonus_token, void* stream);
 
 /*
- * ooo_kv_compact - commit the accepted states (Section 4.4: only states on
+ * ooo_kv_compact - commit the accepted states (Section 4.5: only states on
  * the accepted path enter the committed KV cache).
  *
  * DEVICE pointers.

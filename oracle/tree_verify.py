@@ -12,7 +12,7 @@ with a plain definition, that definition is written out:
 * Section 3 (Target authority, Eq. 1): with greedy decoding, the next
   output token is the target distribution's most likely token, and drafts
   never add output on their own.
-* Section 3 (ToolSpec loop) and Section 4.4 (Verify and commit): all draft
+* Section 3 (ToolSpec loop) and Section 4.5 (Verify and commit): all draft
   continuations form one tree that a single target pass scores; the output
   grows by the longest run of draft tokens that agree with the target's own
   greedy choices, then by the target's choice at the point of disagreement;
@@ -45,8 +45,8 @@ import numpy as np
 
 
 # ----------------------------------------------------------------------------
-# O1: candidate trie (Section 3, ToolSpec loop; Section 4.3, Merge_B keeps a
-# fixed candidate budget, hint lanes first; Section 4.4, one candidate tree)
+# O1: candidate trie (Section 3, ToolSpec loop; Section 4.4, Merge_B keeps a
+# fixed candidate budget, hint lanes first; Section 4.5, one candidate tree)
 
 
 def pack_tree(root_token: int, candidates: Sequence[Sequence[int]], max_nodes: int, max_depth: int) -> Dict:
@@ -114,7 +114,7 @@ def ancestor_masks(parent: np.ndarray, mask_words: int) -> np.ndarray:
 
 # ----------------------------------------------------------------------------
 # O2: attention of every node against the committed prefix and its own
-# ancestors (Section 4.4: the whole tree in one target forward pass, each
+# ancestors (Section 4.5: the whole tree in one target forward pass, each
 # node seeing exactly what sequential decoding of its path would see)
 
 
@@ -193,7 +193,7 @@ def greedy_tokens(logits: np.ndarray) -> Dict[str, np.ndarray]:
 
 
 # ----------------------------------------------------------------------------
-# O4: keep the longest run of agreeing draft tokens (Section 4.4, Verify and commit)
+# O4: keep the longest run of agreeing draft tokens (Section 4.5, Verify and commit)
 
 
 def accept_walk(token: np.ndarray, parent: np.ndarray, ids: np.ndarray) -> Dict:
@@ -218,7 +218,7 @@ def accept_walk(token: np.ndarray, parent: np.ndarray, ids: np.ndarray) -> Dict:
 
 
 # ----------------------------------------------------------------------------
-# O5: commit accepted states into the KV cache (Section 4.4: the cache keeps
+# O5: commit accepted states into the KV cache (Section 4.5: the cache keeps
 # the rows of agreeing nodes, rejected nodes leave no trace)
 
 

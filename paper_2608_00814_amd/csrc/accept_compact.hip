@@ -1,4 +1,4 @@
-// Greedy acceptance and cache compaction (Section 4.4, Verify and commit:
+// Greedy acceptance and cache compaction (Section 4.5, Verify and commit:
 // draft tokens are kept while they match the target's greedy token at their
 // parent, the first mismatch ends the run and the target's own token follows;
 // only the accepted states are committed to the KV cache).

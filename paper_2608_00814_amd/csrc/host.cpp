@@ -29,8 +29,8 @@ extern "C" const char* ooo_last_error(void) { return ooo::g_err; }
 
 extern "C" int ooo_version(void) { return OOO_ABI_VERSION; }
 
-// Candidate trie (Section 3, ToolSpec loop; Section 4.3, fixed candidate
-// budget with hint lanes first; Section 4.4, one candidate tree).  Children
+// Candidate trie (Section 3, ToolSpec loop; Section 4.4, fixed candidate
+// budget with hint lanes first; Section 4.5, one candidate tree).  Children
 // are found through a hash map keyed by (parent, token); the ancestor bitmask
 // of a node is its parent's mask plus its own bit, which is valid because a
 // parent is always created before its children.

@@ -1,4 +1,4 @@
-// Tree-masked attention for one layer (Section 4.4: the target scores the
+// Tree-masked attention for one layer (Section 4.5: the target scores the
 // whole candidate tree in one forward pass; node i sees the committed prefix
 // and its own ancestors, exactly what sequential decoding of its path sees).
 //

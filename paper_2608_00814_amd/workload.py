@@ -9,7 +9,7 @@ plain CPU reference consume what it produces.
 Shapes follow the target models the paper evaluates (Section 5.1): Qwen3,
 Qwen2.5 and Llama families at batch one.  The trie recipes mimic the three
 candidate sources the method merges before one target verification pass
-(Section 4.3: schema-FSM chain, retrieved earlier calls and the sidecar's
+(Section 4.4: schema-FSM chain, retrieved earlier calls and the sidecar's
 re-tokenised hint, hint lanes first).  The paper's datasets (API-Bank,
 ToolAlpaca, BFCL) are not used; seeded draws of the same shapes stand in.
 

@@ -275,6 +275,29 @@ def check_lm_head_library(ov):
     assert int(g2["ids"][0]) == 17 and g2["margin"][0] == 0.0
 
 
+def check_lm_head_closed_forms(ov):
+    """Logits with a closed form: a hidden row c*e_j reads column j of W
+    (one nonzero product per logit); weight rows v*u give logits v*(x.u),
+    so the greedy token is the last row when x.u > 0 and row 0 when x.u < 0."""
+    rs = np.random.default_rng(21)
+    V, H = 203, 48
+    w = rs.normal(size=(V, H))
+    x = np.zeros((3, H))
+    for i, (j, c) in enumerate(((0, 2.0), (17, -0.5), (47, 3.0))):
+        x[i, j] = c
+    logits = ov.lm_head_logits(x, w, rows_per_chunk=50)
+    for i, (j, c) in enumerate(((0, 2.0), (17, -0.5), (47, 3.0))):
+        assert logits[i].tolist() == (c * w[:, j]).tolist()
+    u = rs.normal(size=H)
+    wl = np.arange(V, dtype=np.float64)[:, None] * u[None, :]
+    xs = np.stack([u, -u])
+    g = ov.greedy_tokens(ov.lm_head_logits(xs, wl, rows_per_chunk=64))
+    assert g["ids"].tolist() == [V - 1, 0]
+    uu = float(u @ u)
+    assert abs(g["max_logit"][0] - (V - 1) * uu) <= 1e-9 * V * uu
+    assert abs(g["margin"][0] - uu) <= 1e-9 * V * uu
+
+
 def check_accept_golden(ov):
     data = _load("accept_cases.json")
     token = np.array(data["token"], dtype=np.int32)
@@ -418,6 +441,7 @@ ALL_CHECKS = [
     check_attention_causal_paths,
     check_attention_sdpa_root_and_chain,
     check_attention_closed_forms,
+    check_lm_head_closed_forms,
     check_attention_renumbering,
     check_lm_head_library,
     check_accept_golden,
