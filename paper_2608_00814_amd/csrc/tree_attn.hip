@@ -32,7 +32,8 @@
 namespace ooo {
 namespace {
 
-constexpr int kTile = 64;  // keys per tile
+constexpr int kTile = 64;         // keys per tile
+constexpr int kMaxMaskWords = 16;  // ancestor-mask words per node (up to 1024 nodes)
 
 struct AttnArgs {
   const uint16_t* q;
@@ -63,6 +64,29 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 // "memory" clobber keeps the compiler from moving LDS accesses across it.
 __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
+// LDS DMA of 16 bytes per lane from base + voff (base wave-uniform, voff
+// per lane); lane l's bytes land at LDS byte address lds + 16*l (lds
+// wave-uniform).  Issued through inline asm so the compiler does not track
+// it: it would otherwise make LDS reads of other ring stages wait for every
+// DMA in flight.  Kernels wait for their DMA explicitly (vmcnt, then a
+// barrier).  M0 holds the LDS base; nothing else in these kernels uses M0.
+__device__ __forceinline__ void dma16(const void* base, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(base)
+               : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// max of three floats without the NaN canonicalisation fmaxf implies
+// (scores are finite or -inf)
+__device__ __forceinline__ float max3f(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
 // s_waitcnt vmcnt(n) (n <= 63), leaving the other counters alone.
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -71,33 +95,66 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 
 // LDS ring geometry for one head_dim.  A tile is 64 rows of K and 64 rows of
-// V, each row D bf16 values = D/8 16-byte chunks, stored row-major with
-// chunk c of row r at position c ^ (r % (D/8)).  One 1 KiB DMA instruction
-// copies whole contiguous rows (coalesced in global memory); the XOR
-// swizzle makes reads of one chunk down many rows hit distinct banks.  K
-// tiles of all stages come first, then the V tiles, then the block's
-// queries (padded rows, written once), so every LDS read is a per-lane
-// offset plus a compile-time immediate below 64 KiB.
+// V, each row D bf16 values = D/8 16-byte chunks, stored row-major with the
+// chunks of a row permuted (swz below).  One 1 KiB DMA instruction copies
+// whole contiguous rows (coalesced in global memory).  Every stage of every
+// matrix is its own __shared__ array, so the compiler can tell that a DMA
+// into one stage does not alias reads of another and adds no waits of its
+// own; the kernel waits explicitly (vmcnt, then a barrier).
 template <int D>
 struct Ring {
-  static constexpr int CH = D / 8;           // chunks per row
-  static constexpr int ROWB = 2 * D;         // bytes per row
-  static constexpr int MAT = kTile * ROWB;   // bytes of one K or V tile
-  static constexpr int NS = 3;               // stages
-  static constexpr int VREG = NS * MAT;      // start of the V tiles
-  static constexpr int QREG = 2 * NS * MAT;  // start of the queries
-  static constexpr int QLD = ROWB + 16;      // padded query row
-  static constexpr int DMA_MAT = MAT / 1024; // DMA instructions per matrix
-  static constexpr int RPI = 1024 / ROWB;    // rows per DMA instruction
-  static_assert(2 * DMA_MAT <= 63, "vmcnt range");
+  static constexpr int CH = D / 8;            // chunks per row
+  static constexpr int ROWB = 2 * D;          // bytes per row
+  static constexpr int MAT = kTile * ROWB;    // bytes of one K or V tile
+  static constexpr int NS = 4;                // stages
+  static constexpr int DMA_MAT = MAT / 1024;  // DMA instructions per matrix
+  static constexpr int RPI = 1024 / ROWB;     // rows per DMA instruction
+  static constexpr int GPL = D / 8;           // float4 groups of O^T per lane
+  // Physical chunk of logical chunk c in row r.  For D = 128 the two 2-bit
+  // halves of r % 16 are swapped and XORed in: the K fragment reads (16
+  // lanes, 16 different rows, one chunk) and the V transpose reads (32
+  // lanes, 4 consecutive rows x 4 consecutive chunks) both hit distinct banks.
+  static __device__ __forceinline__ int swz(int r, int c) {
+    if (D == 128) return c ^ (((r & 3) << 2) | ((r >> 2) & 3));
+    return c ^ (r % CH);
+  }
 };
 
-template <int D, int CW>
-__global__ __launch_bounds__(64 * (CW + 2)) __attribute__((amdgpu_waves_per_eu(1, 2)))
-void tree_attn_bf16_kernel(AttnArgs a) {
+// wait until at most `ahead` tiles of `per` DMA instructions are pending
+template <int PER, int MAXA>
+__device__ __forceinline__ void wait_tiles(int ahead) {
+  if (MAXA >= 2 && ahead >= 2) wait_vmcnt<(MAXA >= 2 ? 2 * PER : 0)>();
+  else if (ahead == 1) wait_vmcnt<PER>();
+  else wait_vmcnt<0>();
+}
+
+// Work of one block: RG row groups of 32 query rows.  Without SPLIT one
+// wave per row group reads all 64 keys of every tile; with SPLIT two waves
+// share a row group, each taking one 32-key half of every tile, so that two
+// waves sit on each SIMD and the matrix-core work of one overlaps the vector
+// work of the other; the halves merge their (max, sum, O) through LDS at the
+// end.  Within a wave the loop is software-pipelined: while the matrix cores
+// compute the scores of tile i+1 (S^T = K Q^T), the vector units turn the
+// scores of tile i into probabilities; the P V product of tile i overlaps the
+// row max of tile i+1.  LDS reads are issued one phase ahead of their use.
+// Every wave issues its share of each tile's DMA.
+template <int D, int RG, bool SPLIT>
+__global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kernel(AttnArgs a) {
   using R = Ring<D>;
-  constexpr int BM = 32 * CW;  // query rows per block
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[R::QREG + BM * R::QLD];
+  constexpr int NW = RG * (SPLIT ? 2 : 1);  // waves
+  constexpr int NH = SPLIT ? 1 : 2;         // 32-key halves per wave and tile
+  constexpr int BM = 32 * RG;               // query rows per block
+  constexpr int PM = R::DMA_MAT / NW;       // DMA instructions per wave per matrix
+  constexpr int PER = 2 * PM;               // ... per tile
+  static_assert(R::DMA_MAT % NW == 0, "DMA split");
+  static_assert(2 * PER <= 63, "vmcnt range");
+  static_assert(R::GPL % 4 == 0, "merge layout");
+  __shared__ __attribute__((aligned(1024))) uint8_t k0[R::MAT], k1[R::MAT], k2[R::MAT], k3[R::MAT];
+  __shared__ __attribute__((aligned(1024))) uint8_t v0[R::MAT], v1[R::MAT], v2[R::MAT], v3[R::MAT];
+  // ancestor-mask words of the block's rows (a wave reads only its own rows)
+  __shared__ uint64_t mwords[RG * 32 * kMaxMaskWords];
+  uint8_t* const kst[R::NS] = {k0, k1, k2, k3};
+  uint8_t* const vst[R::NS] = {v0, v1, v2, v3};
 
   const int total = a.Hkv * a.row_blocks * a.splits;
   int w = blockIdx.x;
@@ -111,71 +168,90 @@ void tree_attn_bf16_kernel(AttnArgs a) {
   const int ntiles = t_end - t_begin;  // >= 1 because splits <= tiles
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-
-  if (wave >= CW) {
-    // ------------------------------------------------- loaders: K (CW), V (CW+1)
-    const bool is_v = wave == CW + 1;
-    const uint16_t* src = (is_v ? a.v : a.k) + (size_t)g * a.cap * D;
-    uint8_t* dst0 = lds + (is_v ? R::VREG : 0);
-    auto issue = [&](int t, int stage) {
-      int row0, limit;
-      if (t < a.tiles_prefix) {
-        row0 = t * kTile;
-        limit = a.P;
-      } else {
-        row0 = a.P + (t - a.tiles_prefix) * kTile;
-        limit = a.P + a.N;
-      }
-      uint8_t* dst = dst0 + stage * R::MAT;
-#pragma unroll
-      for (int j = 0; j < R::DMA_MAT; ++j) {
-        // lane = (row within the instruction, swizzled chunk); rows past the
-        // limit re-read the last valid row (masked keys, zero probability)
-        const int r = j * R::RPI + lane / R::CH;
-        const int c = (lane % R::CH) ^ (r % R::CH);
-        const size_t off = (size_t)min(row0 + r, limit - 1) * D + c * 8;
-        __builtin_amdgcn_global_load_lds(OOO_GLB(src + off), OOO_LDS(dst + j * 1024), 16, 0, 0);
-      }
-    };
-    issue(t_begin, 0);
-    if (ntiles > 1) issue(t_begin + 1, 1);
-    for (int i = 0; i < ntiles; ++i) {
-      if (i + 1 < ntiles) wait_vmcnt<R::DMA_MAT>();  // tile i landed, i+1 may be in flight
-      else wait_vmcnt<0>();
-      wg_barrier();
-      if (i + 2 < ntiles) issue(t_begin + i + 2, (i + 2) % R::NS);
-    }
-    return;
-  }
-
-  // ------------------------------------------------------------------ compute
+  const int rg = wave % RG, kh0 = SPLIT ? wave / RG : 0;
   const int c = lane & 31, u = lane >> 5;
-  const int row = rb * BM + wave * 32 + c;
+  uint64_t* const mrow = mwords + (rg * 32 + c) * kMaxMaskWords;
+  const int row = rb * BM + rg * 32 + c;
   const bool row_ok = row < a.M;
   const int rr = row_ok ? row : a.M - 1;
   const int node = rr / a.G;
   const int head = g * a.G + (rr - node * a.G);
+  const uint16_t* const kg = a.k + (size_t)g * a.cap * D;
+  const uint16_t* const vg = a.v + (size_t)g * a.cap * D;
 
-  // this wave's 32 query rows into its private LDS slice (padded rows)
-  const uint32_t qb = R::QREG + (wave * 32 + c) * R::QLD + u * 16;  // + 32*dk
+  // Q^T fragments (B operand of S^T = K Q^T): row c, k = 16dk + 8u .. +8
+  bf16x8 qf[D / 16];
   {
     const uint16_t* qrow = a.q + ((size_t)node * a.Hq + head) * D;
 #pragma unroll
-    for (int dk = 0; dk < D / 16; ++dk)
-      *reinterpret_cast<u32x4*>(lds + qb + 32 * dk) = ld16(qrow + 16 * dk + 8 * u);
+    for (int dk = 0; dk < D / 16; ++dk) qf[dk] = as_bf16x8(ld16(qrow + 16 * dk + 8 * u));
   }
-  // ancestor-mask word of the next tree tile this split will see
-  int next_tt = t_begin > a.tiles_prefix ? t_begin - a.tiles_prefix : 0;
-  uint64_t mnext = a.mask[(size_t)node * a.W + next_tt];
 
-  // per-lane LDS byte offsets (loop invariant).  K fragment (half kt, k-step
-  // dk): chunk 2dk+u of row sigma(c)+32kt.  V^T transpose-read source (for
-  // column block dt, key step ks, half h): row 16ks+4h+8(g16/2)+li/4, columns
-  // 32dt+16(g16%2)+4(li%4) .. +3.
+  auto tile_rows = [&](int t, int& row0, int& limit) {
+    if (t < a.tiles_prefix) {
+      row0 = t * kTile;
+      limit = a.P;
+    } else {
+      row0 = a.P + (t - a.tiles_prefix) * kTile;
+      limit = a.P + a.N;
+    }
+  };
+  // DMA instruction j of a matrix copies rows RPI*j .. +RPI: lane = (row
+  // within the instruction, physical chunk), so it reads the logical chunk
+  // swz(r, physical) of row r.  Interior tiles use the per-lane byte offsets
+  // below from a uniform tile base; a tile that crosses the end of its
+  // region clamps rows past it to the last valid row (masked keys, zero
+  // probability).
+  const uint32_t wave_u = __builtin_amdgcn_readfirstlane(wave);
+  uint32_t dvoff[PM];
+#pragma unroll
+  for (int i = 0; i < PM; ++i) {
+    const int r = (i * NW + wave) * R::RPI + lane / R::CH;
+    dvoff[i] = r * R::ROWB + R::swz(r, lane % R::CH) * 16;
+  }
+  auto issue = [&](int t, auto stage_c) {
+    constexpr int ST = decltype(stage_c)::value;
+    int row0, limit;
+    tile_rows(t, row0, limit);
+    const uint16_t* kb = kg + (size_t)row0 * D;
+    const uint16_t* vb = vg + (size_t)row0 * D;
+    const uint32_t kl = lds_addr(kst[ST]) + wave_u * 1024, vl = lds_addr(vst[ST]) + wave_u * 1024;
+    if (row0 + kTile <= limit) {
+#pragma unroll
+      for (int i = 0; i < PM; ++i) dma16(kb, dvoff[i], kl + i * NW * 1024);
+#pragma unroll
+      for (int i = 0; i < PM; ++i) dma16(vb, dvoff[i], vl + i * NW * 1024);
+    } else {
+#pragma unroll
+      for (int i = 0; i < PM; ++i) {
+        const int r = (i * NW + wave) * R::RPI + lane / R::CH;
+        const int rc = min(r, limit - 1 - row0);
+        const uint32_t vo = rc * R::ROWB + R::swz(r, lane % R::CH) * 16;
+        dma16(kb, vo, kl + i * NW * 1024);
+        dma16(vb, vo, vl + i * NW * 1024);
+      }
+    }
+  };
+
+  // The mask words go through LDS so that no global load is pending inside
+  // the tile loop, where a wait for it would also wait for the tile DMA.
+  if (kh0 == 0)
+    for (int wd = u; wd < a.W; wd += 2) mrow[wd] = a.mask[(size_t)node * a.W + wd];
+
+  issue(t_begin, std::integral_constant<int, 0>{});
+  if (ntiles > 1) issue(t_begin + 1, std::integral_constant<int, 1>{});
+  if (ntiles > 2) issue(t_begin + 2, std::integral_constant<int, 2>{});
+
+  // Per-lane LDS byte offsets (loop invariant).  K fragment (half kh,
+  // k-step dk): logical chunk 2dk+u of row sigma(c) + 32kh (the physical
+  // chunk only depends on the row mod 16).  V^T transpose-read source
+  // (column block dt, key step ks, half h): row 16ks + 4h + 8(g16/2) + li/4,
+  // columns 32dt + 16(g16%2) + 4(li%4) .. +3.
   const int krow = sigma(c);
   uint32_t koff[D / 16];
 #pragma unroll
-  for (int dk = 0; dk < D / 16; ++dk) koff[dk] = krow * R::ROWB + (((2 * dk + u) ^ (krow % R::CH)) << 4);
+  for (int dk = 0; dk < D / 16; ++dk)
+    koff[dk] = (krow + 32 * kh0) * R::ROWB + (R::swz(krow, 2 * dk + u) << 4);
   const int g16 = lane >> 4, li = lane & 15;
   uint32_t voff[D / 32][2];
 #pragma unroll
@@ -184,7 +260,7 @@ void tree_attn_bf16_kernel(AttnArgs a) {
     for (int h = 0; h < 2; ++h) {
       const int vr = 4 * h + 8 * (g16 >> 1) + (li >> 2);  // key row within a 16-row block
       const int col = 32 * dt + 16 * (g16 & 1) + 4 * (li & 3);
-      voff[dt][h] = R::VREG + vr * R::ROWB + (((col >> 3) ^ (vr % R::CH)) << 4) + (col & 7) * 2;
+      voff[dt][h] = (vr + 32 * kh0) * R::ROWB + (R::swz(vr, col >> 3) << 4) + (col & 7) * 2;
     }
 
   f32x16 oacc[D / 32];
@@ -192,124 +268,248 @@ void tree_attn_bf16_kernel(AttnArgs a) {
   for (int dt = 0; dt < D / 32; ++dt) oacc[dt] = f32x16{};
   float m_run = -INFINITY, l_run = 0.f;
 
-  auto tile = [&](int i, auto stage_c) {
+  // K fragments of k-steps 4b .. 4b+3 for the wave's halves
+  auto kread = [&](auto stage_c, int b, bf16x8 (&kf)[NH][4]) {
     constexpr int ST = decltype(stage_c)::value;
-    const int t = t_begin + i;
-    wg_barrier();  // tile t is in stage ST
-    const uint8_t* Ks = lds + ST * R::MAT;
-
-    // S^T = K Q^T for both 32-key halves first, so the softmax of half A
-    // (VALU) can run while the matrix cores still work on half B.
-    f32x16 sh[2] = {f32x16{}, f32x16{}};
+    const uint8_t* Ks = kst[ST];
 #pragma unroll
-    for (int b4 = 0; b4 < D / 64; ++b4) {
-      bf16x8 k0[4], k1[4], qq[4];
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int dk = 4 * b4 + j;
-        qq[j] = as_bf16x8(*reinterpret_cast<const u32x4*>(lds + qb + 32 * dk));
-        k0[j] = as_bf16x8(*reinterpret_cast<const u32x4*>(Ks + koff[dk]));
-        k1[j] = as_bf16x8(*reinterpret_cast<const u32x4*>(Ks + koff[dk] + 32 * R::ROWB));
+      for (int hf = 0; hf < NH; ++hf)
+        kf[hf][j] = as_bf16x8(*reinterpret_cast<const u32x4*>(Ks + koff[4 * b + j] + 32 * hf * R::ROWB));
+  };
+  auto qk_mfma = [&](int b, const bf16x8 (&kf)[NH][4], f32x16 (&acc)[NH]) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int hf = 0; hf < NH; ++hf) acc[hf] = mfma32(kf[hf][j], qf[4 * b + j], acc[hf]);
+  };
+  // V^T fragments of local key step ks (16 keys of the wave's range)
+  auto vread = [&](auto stage_c, int ks, bf16x8 (&vv)[D / 32]) {
+    constexpr int ST = decltype(stage_c)::value;
+    const uint8_t* Vs = vst[ST];
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) {
+      u32x2 lohi[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const uint8_t* p = Vs + voff[dt][h] + ks * 16 * R::ROWB;
+        lohi[h] = __builtin_bit_cast(
+            u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((i16x4 __attribute__((address_space(3)))*)OOO_LDS(p)));
       }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        sh[0] = mfma32(k0[j], qq[j], sh[0]);
-        sh[1] = mfma32(k1[j], qq[j], sh[1]);
-      }
+      vv[dt] = as_bf16x8(u32x4{lohi[0][0], lohi[0][1], lohi[1][0], lohi[1][1]});
     }
+  };
+  auto pv_mfma = [&](const bf16x8 (&vv)[D / 32], const bf16x8& p) {
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) oacc[dt] = mfma32(vv[dt], p, oacc[dt]);
+  };
+  // probabilities of one 32-key half in B-operand order; returns their sum
+  auto probs_half = [&](const f32x16& acc, float m_use, bf16x8& p0, bf16x8& p1) {
+    float psum = 0.f;
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) {
+      float p[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        p[e] = __builtin_amdgcn_exp2f(fmaf(acc[8 * k2 + e], a.scale_log2e, -m_use));
+        psum += p[e];
+      }
+      u32x4 pk;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) pk[e] = pack_bf16x2(p[2 * e], p[2 * e + 1]);
+      (k2 == 0 ? p0 : p1) = as_bf16x8(pk);
+    }
+    return psum;
+  };
+  // Mask tile t's scores (tree tiles and ragged tails only).  Lane value j
+  // of half hf is key 32(kh0+hf) + 16*(j/8) + 8u + j%8 of the tile.
+  auto apply_mask = [&](int t, f32x16 (&acc)[NH]) {
+    int row0, limit;
+    tile_rows(t, row0, limit);
     const bool tree = t >= a.tiles_prefix;
-    const int row0 = tree ? a.P + (t - a.tiles_prefix) * kTile : t * kTile;
-    const int limit = tree ? a.P + a.N : a.P;
-    const bool masked = tree || row0 + kTile > limit;
-    uint64_t mw = ~0ull;
-    if (tree) {
-      mw = mnext;
-      next_tt = min(next_tt + 1, a.W - 1);
-      mnext = a.mask[(size_t)node * a.W + next_tt];
-    }
-
+    if (tree || row0 + kTile > limit) {
+      const uint64_t mw = tree ? mrow[t - a.tiles_prefix] : ~0ull;
 #pragma unroll
-    for (int hf = 0; hf < 2; ++hf) {
-      // lane's value j of this half is key 32hf + 16*(j/8) + 8u + j%8 of the tile
-      float sv[16];
-#pragma unroll
-      for (int j = 0; j < 16; ++j) sv[j] = sh[hf][j];
-      if (masked) {
+      for (int hf = 0; hf < NH; ++hf)
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
-          const int off = 32 * hf + 16 * (j / 8) + 8 * u + (j % 8);
+          const int off = 32 * (kh0 + hf) + 16 * (j / 8) + 8 * u + (j % 8);
           const bool ok = (row0 + off < limit) && ((mw >> off) & 1ull);
-          if (!ok) sv[j] = -INFINITY;
+          if (!ok) acc[hf][j] = -INFINITY;
         }
+    }
+  };
+  // row max of a tile's scores over the wave's keys, in log2 units
+  auto row_max = [&](const f32x16 (&acc)[NH]) {
+    float mh[NH];
+#pragma unroll
+    for (int hf = 0; hf < NH; ++hf) {
+      float m = max3f(acc[hf][0], acc[hf][1], acc[hf][2]);
+#pragma unroll
+      for (int j = 3; j < 15; j += 2) m = max3f(m, acc[hf][j], acc[hf][j + 1]);
+      mh[hf] = max3f(m, acc[hf][15], -INFINITY);
+    }
+    const float mx = NH == 2 ? max3f(mh[0], mh[NH - 1], -INFINITY) : mh[0];
+    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+    return max3f(__uint_as_float(sw[0]), __uint_as_float(sw[1]), -INFINITY) * a.scale_log2e;
+  };
+  // Lazy rescaling: the reference max m_run moves only when some row of the
+  // wave grows by more than 2^8, so probabilities stay <= 256 (fine for fp32
+  // sums and bf16 operands) and O, l are rescaled rarely.
+  auto rescale = [&](float mx) {
+    if (__any(mx > m_run + 8.f)) {
+      const float m_new = __builtin_fmaxf(m_run, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - (m_new == -INFINITY ? 0.f : m_new));
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < D / 32; ++dt) oacc[dt] *= alpha;
+      m_run = m_new;
+    }
+  };
+
+  // prologue: scores, mask and max of the first tile
+  f32x16 sa_buf[NH], sb_buf[NH];
+  wait_tiles<PER, 2>(min(2, ntiles - 1));
+  wg_barrier();
+  {
+    bf16x8 kf[NH][4];
+#pragma unroll
+    for (int hf = 0; hf < NH; ++hf) sa_buf[hf] = f32x16{};
+#pragma unroll
+    for (int b = 0; b < D / 64; ++b) {
+      kread(std::integral_constant<int, 0>{}, b, kf);
+      qk_mfma(b, kf, sa_buf);
+    }
+  }
+  apply_mask(t_begin, sa_buf);
+  rescale(row_max(sa_buf));
+
+  // One pipeline step: tile i is in stage SA with its scores in scur, tile
+  // i+1 (if NEXT) in stage SB, its scores go to snxt; tile i+3 is issued
+  // into SD, the stage tile i-1 used.  The row max of tile i+1 is taken
+  // before masking; a masked tile (tree tiles, ragged tails) takes it again
+  // after the mask.  Phases are separated by scheduling barriers.
+  auto step = [&](int i, auto sa, auto sb, auto sd, auto next_c, f32x16 (&scur)[NH], f32x16 (&snxt)[NH]) {
+    constexpr bool NEXT = decltype(next_c)::value;
+    if (NEXT) {
+      wait_tiles<PER, 1>(min(1, ntiles - 2 - i));  // this wave's share of tile i+1 landed
+      wg_barrier();                                // ... and every other wave's
+      if (i + 3 < ntiles) issue(t_begin + i + 3, sd);
+    }
+    const float m_use = m_run == -INFINITY ? 0.f : m_run;
+    bf16x8 pf[2 * NH];
+    bf16x8 vv0[D / 32], vv1[D / 32];
+    if (NEXT) {
+      bf16x8 kf[NH][4];
+      __builtin_amdgcn_sched_barrier(0);
+      kread(sb, 0, kf);
+      vread(sa, 0, vv0);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int hf = 0; hf < NH; ++hf) snxt[hf] = f32x16{};
+      qk_mfma(0, kf, snxt);
+      float ps = probs_half(scur[0], m_use, pf[0], pf[1]);
+      kread(sb, 1, kf);
+      __builtin_amdgcn_sched_barrier(0);
+      qk_mfma(1, kf, snxt);
+      if (NH == 2) ps += probs_half(scur[NH - 1], m_use, pf[2 * NH - 2], pf[2 * NH - 1]);
+      vread(sa, 1, vv1);
+      l_run += ps;
+      __builtin_amdgcn_sched_barrier(0);
+      pv_mfma(vv0, pf[0]);
+      if (NH == 2) vread(sa, 2, vv0);
+      __builtin_amdgcn_sched_barrier(0);
+      pv_mfma(vv1, pf[1]);
+      if (NH == 2) vread(sa, 3, vv1);
+      float mx = row_max(snxt);
+      __builtin_amdgcn_sched_barrier(0);
+      if (NH == 2) {
+        pv_mfma(vv0, pf[2 * NH - 2]);
+        pv_mfma(vv1, pf[2 * NH - 1]);
       }
-      float mx = sv[0];
-#pragma unroll
-      for (int j = 1; j < 16; ++j) mx = __builtin_fmaxf(mx, sv[j]);
-      {
-        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
-        mx = __builtin_fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * a.scale_log2e;  // log2 units
+      __builtin_amdgcn_sched_barrier(0);
+      int row0, limit;
+      tile_rows(t_begin + i + 1, row0, limit);
+      if (t_begin + i + 1 >= a.tiles_prefix || row0 + kTile > limit) {
+        apply_mask(t_begin + i + 1, snxt);
+        mx = row_max(snxt);
       }
-      // Lazy rescaling: the reference max m_run moves only when some row of
-      // the wave grows by more than 2^8, so probabilities stay <= 256 (fine
-      // for fp32 sums and bf16 operands) and O, l are rescaled rarely.
-      if (__any(mx > m_run + 8.f)) {
-        const float m_new = __builtin_fmaxf(m_run, mx);
-        const float alpha = __builtin_amdgcn_exp2f(m_run - (m_new == -INFINITY ? 0.f : m_new));
-        l_run *= alpha;
+      rescale(mx);
+    } else {
+      float ps = 0.f;
 #pragma unroll
-        for (int dt = 0; dt < D / 32; ++dt) oacc[dt] *= alpha;
-        m_run = m_new;
-      }
-      const float m_use = m_run == -INFINITY ? 0.f : m_run;
-      float psum = 0.f;
+      for (int hf = 0; hf < NH; ++hf) ps += probs_half(scur[hf], m_use, pf[2 * hf], pf[2 * hf + 1]);
+      l_run += ps;
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        sv[j] = __builtin_amdgcn_exp2f(fmaf(sv[j], a.scale_log2e, -m_use));
-        psum += sv[j];
-      }
-      l_run += psum;
-      bf16x8 pf[2];
-#pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2) {
-        u32x4 pk;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) pk[e] = pack_bf16x2(sv[8 * k2 + 2 * e], sv[8 * k2 + 2 * e + 1]);
-        pf[k2] = as_bf16x8(pk);
-      }
-      // O^T += V^T P^T for this half (key steps ks = 2hf, 2hf+1).  V^T
-      // fragments come from the row-major V tile through the LDS transpose
-      // read: within each 16-lane group, source lane 4k+q points at key row
-      // k, columns 4q..4q+3, and lane i receives column i of the four rows.
-#pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2) {
-        const int ks = 2 * hf + k2;
-        bf16x8 vv[D / 32];
-#pragma unroll
-        for (int dt = 0; dt < D / 32; ++dt) {
-          u32x2 lohi[2];
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const uint8_t* p = lds + voff[dt][h] + ST * R::MAT + ks * 16 * R::ROWB;
-            lohi[h] = __builtin_bit_cast(
-                u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((i16x4 __attribute__((address_space(3)))*)OOO_LDS(p)));
-          }
-          vv[dt] = as_bf16x8(u32x4{lohi[0][0], lohi[0][1], lohi[1][0], lohi[1][1]});
-        }
-#pragma unroll
-        for (int dt = 0; dt < D / 32; ++dt) oacc[dt] = mfma32(vv[dt], pf[k2], oacc[dt]);
+      for (int ks = 0; ks < 2 * NH; ++ks) {
+        vread(sa, ks, vv0);
+        pv_mfma(vv0, pf[ks]);
       }
     }
   };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  using YES = std::integral_constant<bool, true>;
+  using NO = std::integral_constant<bool, false>;
   int i = 0;
-  for (; i + R::NS <= ntiles; i += R::NS) {
-    tile(i, std::integral_constant<int, 0>{});
-    tile(i + 1, std::integral_constant<int, 1>{});
-    tile(i + 2, std::integral_constant<int, 2>{});
+  for (; i + 4 < ntiles; i += 4) {  // steps i .. i+3 all have a next tile
+    step(i, I0{}, I1{}, I3{}, YES{}, sa_buf, sb_buf);
+    step(i + 1, I1{}, I2{}, I0{}, YES{}, sb_buf, sa_buf);
+    step(i + 2, I2{}, I3{}, I1{}, YES{}, sa_buf, sb_buf);
+    step(i + 3, I3{}, I0{}, I2{}, YES{}, sb_buf, sa_buf);
   }
-  if (i < ntiles) tile(i, std::integral_constant<int, 0>{});
-  if (i + 1 < ntiles) tile(i + 1, std::integral_constant<int, 1>{});
+  // 1..4 steps remain; the last has no next tile
+  const int rem = ntiles - i;
+  if (rem == 1) {
+    step(i, I0{}, I1{}, I3{}, NO{}, sa_buf, sb_buf);
+  } else if (rem == 2) {
+    step(i, I0{}, I1{}, I3{}, YES{}, sa_buf, sb_buf);
+    step(i + 1, I1{}, I2{}, I0{}, NO{}, sb_buf, sa_buf);
+  } else if (rem == 3) {
+    step(i, I0{}, I1{}, I3{}, YES{}, sa_buf, sb_buf);
+    step(i + 1, I1{}, I2{}, I0{}, YES{}, sb_buf, sa_buf);
+    step(i + 2, I2{}, I3{}, I1{}, NO{}, sa_buf, sb_buf);
+  } else {
+    step(i, I0{}, I1{}, I3{}, YES{}, sa_buf, sb_buf);
+    step(i + 1, I1{}, I2{}, I0{}, YES{}, sb_buf, sa_buf);
+    step(i + 2, I2{}, I3{}, I1{}, YES{}, sa_buf, sb_buf);
+    step(i + 3, I3{}, I0{}, I2{}, NO{}, sb_buf, sa_buf);
+  }
 
-  const float l_tot = l_run + shfl_xor_f(l_run, 32);
+  float l_tot = l_run + shfl_xor_f(l_run, 32);
+  if (SPLIT) {
+    // Merge the two key halves of each row group.  The ring is free once
+    // every wave is past its last tile (the last wait was vmcnt 0).  O^T
+    // group q of a lane (4 floats) goes to stage array q / (GPL/4).
+    constexpr int QPA = R::GPL / 4;
+    __syncthreads();
+    if (kh0 == 1) {
+#pragma unroll
+      for (int q = 0; q < R::GPL; ++q) {
+        const f32x4 v4 = {oacc[q / 4][4 * (q % 4)], oacc[q / 4][4 * (q % 4) + 1], oacc[q / 4][4 * (q % 4) + 2],
+                          oacc[q / 4][4 * (q % 4) + 3]};
+        *reinterpret_cast<f32x4*>(kst[q / QPA] + ((rg * QPA + q % QPA) * 64 + lane) * 16) = v4;
+      }
+      *reinterpret_cast<f32x2_t*>(v0 + (rg * 64 + lane) * 8) = f32x2_t{m_run, l_tot};
+    }
+    __syncthreads();
+    if (kh0 == 1) return;
+    const f32x2_t ml = *reinterpret_cast<const f32x2_t*>(v0 + (rg * 64 + lane) * 8);
+    const float mn = __builtin_fmaxf(m_run, ml[0]);
+    const float base = mn == -INFINITY ? 0.f : mn;
+    const float a0 = __builtin_amdgcn_exp2f(m_run - base), a1 = __builtin_amdgcn_exp2f(ml[0] - base);
+    l_tot = l_tot * a0 + ml[1] * a1;
+    m_run = mn;
+#pragma unroll
+    for (int q = 0; q < R::GPL; ++q) {
+      const f32x4 o1 = *reinterpret_cast<const f32x4*>(kst[q / QPA] + ((rg * QPA + q % QPA) * 64 + lane) * 16);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) oacc[q / 4][4 * (q % 4) + e] = oacc[q / 4][4 * (q % 4) + e] * a0 + o1[e] * a1;
+    }
+  }
   if (!row_ok) return;
   // lane holds output columns d = 32*dt + 8*(j/4) + 4u + j%4 of its row
   if (a.splits == 1) {
@@ -343,12 +543,13 @@ void tree_attn_bf16_kernel(AttnArgs a) {
   }
 }
 
-// Merge the splits of each query row, online over the splits:
-// O = sum_s 2^(m_s - m) O_s / sum_s 2^(m_s - m) l_s.  A split that saw no
-// allowed key has m_s = -inf, l_s = 0 and O_s = 0 and gets weight zero.
-// Every split's loads are independent of the running state, so the unrolled
-// loop keeps many of them in flight.
-template <int D>
+// Merge the splits of each query row:
+// O = sum_s 2^(m_s - m) O_s / sum_s 2^(m_s - m) l_s with m = max_s m_s.
+// A split that saw no allowed key has m_s = -inf, l_s = 0 and O_s = 0 and
+// gets weight zero.  Every load is issued before any arithmetic (one round
+// trip to memory): splits past the count re-read the last split and get
+// weight zero.
+template <int D, int SMAX>
 __global__ __launch_bounds__(256) void tree_attn_combine_kernel(AttnArgs a) {
   constexpr int TPR = D / 4;  // threads per row, 4 columns each
   const int gr = blockIdx.x * (256 / TPR) + threadIdx.x / TPR;
@@ -357,19 +558,25 @@ __global__ __launch_bounds__(256) void tree_attn_combine_kernel(AttnArgs a) {
   const int d0 = (threadIdx.x % TPR) * 4;
   const size_t stride = (size_t)a.Hkv * a.Mpad;  // rows between consecutive splits
   const size_t row0 = (size_t)g * a.Mpad + r;
-  float mrun = -INFINITY, den = 0.f;
+  f32x2_t ml[SMAX];
+  f32x4 o[SMAX];
+#pragma unroll
+  for (int s = 0; s < SMAX; ++s) {
+    const size_t prow = row0 + (size_t)min(s, a.splits - 1) * stride;
+    ml[s] = *reinterpret_cast<const f32x2_t*>(a.part_ml + prow * 2);
+    o[s] = *reinterpret_cast<const f32x4*>(a.part_o + prow * D + d0);
+  }
+  float m = -INFINITY;
+#pragma unroll
+  for (int s = 0; s < SMAX; ++s) m = __builtin_fmaxf(m, ml[s][0]);
+  const float base = m == -INFINITY ? 0.f : m;
+  float den = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 8
-  for (int s = 0; s < a.splits; ++s) {
-    const size_t prow = row0 + s * stride;
-    const float m = a.part_ml[prow * 2], l = a.part_ml[prow * 2 + 1];
-    const f32x4 o = *reinterpret_cast<const f32x4*>(a.part_o + prow * D + d0);
-    const float mn = __builtin_fmaxf(mrun, m);
-    const float base = mn == -INFINITY ? 0.f : mn;
-    const float c_old = __builtin_amdgcn_exp2f(mrun - base), c_new = __builtin_amdgcn_exp2f(m - base);
-    den = den * c_old + l * c_new;
-    acc = acc * c_old + o * c_new;
-    mrun = mn;
+#pragma unroll
+  for (int s = 0; s < SMAX; ++s) {
+    const float wgt = s < a.splits ? __builtin_amdgcn_exp2f(ml[s][0] - base) : 0.f;
+    den += wgt * ml[s][1];
+    acc += wgt * o[s];
   }
   const float inv = 1.f / den;
   const int node = r / a.G, head = g * a.G + r % a.G;
@@ -425,7 +632,7 @@ Plan make_plan(int N, int Hq, int Hkv, int D, int P, ooo_dtype dt) {
   if (dt != OOO_BF16) return p;
   const int G = Hq / Hkv;
   const int M = N * G;
-  p.waves = M <= 64 ? 2 : 4;
+  p.waves = M <= 64 ? 2 : 4;  // waves of 32 query rows
   const int BM = 32 * p.waves;
   p.row_blocks = (M + BM - 1) / BM;
   p.Mpad = p.row_blocks * BM;
@@ -518,18 +725,25 @@ extern "C" int ooo_tree_attn(const void* q, const void* k_cache, const void* v_c
     }
     const dim3 grid(n_kv_heads * p.row_blocks * p.splits);
     if (head_dim == 128) {
-      if (p.waves == 2) tree_attn_bf16_kernel<128, 2><<<grid, 256, 0, st>>>(a);
-      else tree_attn_bf16_kernel<128, 4><<<grid, 384, 0, st>>>(a);
+      if (p.waves == 2) tree_attn_bf16_kernel<128, 2, false><<<grid, 128, 0, st>>>(a);
+      else tree_attn_bf16_kernel<128, 4, false><<<grid, 256, 0, st>>>(a);
     } else {
-      if (p.waves == 2) tree_attn_bf16_kernel<64, 2><<<grid, 256, 0, st>>>(a);
-      else tree_attn_bf16_kernel<64, 4><<<grid, 384, 0, st>>>(a);
+      if (p.waves == 2) tree_attn_bf16_kernel<64, 2, false><<<grid, 128, 0, st>>>(a);
+      else tree_attn_bf16_kernel<64, 4, false><<<grid, 256, 0, st>>>(a);
     }
     if (p.splits > 1) {
       const int rows = n_kv_heads * a.M;
       const int rows_per_block = 256 / (head_dim / 4);
       const dim3 cgrid((rows + rows_per_block - 1) / rows_per_block);
-      if (head_dim == 128) tree_attn_combine_kernel<128><<<cgrid, 256, 0, st>>>(a);
-      else tree_attn_combine_kernel<64><<<cgrid, 256, 0, st>>>(a);
+      if (head_dim == 128) {
+        if (p.splits <= 8) tree_attn_combine_kernel<128, 8><<<cgrid, 256, 0, st>>>(a);
+        else if (p.splits <= 16) tree_attn_combine_kernel<128, 16><<<cgrid, 256, 0, st>>>(a);
+        else tree_attn_combine_kernel<128, 32><<<cgrid, 256, 0, st>>>(a);
+      } else {
+        if (p.splits <= 8) tree_attn_combine_kernel<64, 8><<<cgrid, 256, 0, st>>>(a);
+        else if (p.splits <= 16) tree_attn_combine_kernel<64, 16><<<cgrid, 256, 0, st>>>(a);
+        else tree_attn_combine_kernel<64, 32><<<cgrid, 256, 0, st>>>(a);
+      }
     }
   }
   const hipError_t e = hipGetLastError();
