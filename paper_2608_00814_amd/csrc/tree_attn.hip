@@ -46,8 +46,8 @@ struct AttnArgs {
   int Hq, Hkv, G, M;
   float scale_log2e;
   uint16_t* out;
-  float* part_o;
-  float* part_ml;
+  uint32_t* part_o;  // fp16 normalised partial outputs (fragment order)
+  float* part_ml;    // per partial row: max, sum, scale, unused
   int splits, row_blocks, Mpad, tiles_prefix, tiles_total;
 };
 
@@ -238,9 +238,9 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
   if (kh0 == 0)
     for (int wd = u; wd < a.W; wd += 2) mrow[wd] = a.mask[(size_t)node * a.W + wd];
 
+  // Only the first tile is requested up front: when every block asks for
+  // several tiles at once, each block's first tile lands late.
   issue(t_begin, std::integral_constant<int, 0>{});
-  if (ntiles > 1) issue(t_begin + 1, std::integral_constant<int, 1>{});
-  if (ntiles > 2) issue(t_begin + 2, std::integral_constant<int, 2>{});
 
   // Per-lane LDS byte offsets (loop invariant).  K fragment (half kh,
   // k-step dk): logical chunk 2dk+u of row sigma(c) + 32kh (the physical
@@ -370,8 +370,10 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
 
   // prologue: scores, mask and max of the first tile
   f32x16 sa_buf[NH], sb_buf[NH];
-  wait_tiles<PER, 2>(min(2, ntiles - 1));
+  wait_vmcnt<0>();
   wg_barrier();
+  if (ntiles > 1) issue(t_begin + 1, std::integral_constant<int, 1>{});
+  if (ntiles > 2) issue(t_begin + 2, std::integral_constant<int, 2>{});
   {
     bf16x8 kf[NH][4];
 #pragma unroll
@@ -526,64 +528,97 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
       }
     }
   } else {
-    const size_t prow = ((size_t)s * a.Hkv + g) * a.Mpad + row;
-    float* po = a.part_o + prow * D;
+    // Split partial: the normalised output O/l (a convex combination of V
+    // rows) in fp16, times 2^-e per row so that its largest magnitude lies
+    // in [0.5, 1), plus (max, sum, 2^e) in fp32.  Fragment order: for each
+    // (split, KV head, 32-row block) the lanes' O^T groups f = 4dt + q4 are
+    // stored in pairs [f/2][lane] as 8 halves, so every store (and every
+    // load of the combine) covers 1 KiB contiguously.
+    float amax = 0.f;
 #pragma unroll
-    for (int dt = 0; dt < D / 32; ++dt) {
+    for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        f32x4 v4 = {oacc[dt][4 * q4], oacc[dt][4 * q4 + 1], oacc[dt][4 * q4 + 2], oacc[dt][4 * q4 + 3]};
-        *reinterpret_cast<f32x4*>(po + 32 * dt + 8 * q4 + 4 * u) = v4;
-      }
+      for (int j = 0; j < 16; j += 2) amax = max3f(amax, __builtin_fabsf(oacc[dt][j]), __builtin_fabsf(oacc[dt][j + 1]));
+    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(amax), __float_as_uint(amax), false, false);
+    amax = max3f(__uint_as_float(sw[0]), __uint_as_float(sw[1]), 0.f);
+    const float inv_l = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    const int ex = __builtin_amdgcn_frexp_expf(amax * inv_l);
+    const float mul = __builtin_amdgcn_ldexpf(inv_l, -ex);
+    const size_t blk = ((size_t)s * a.Hkv + g) * (a.Mpad / 32) + (row >> 5);
+    u32x4* po = reinterpret_cast<u32x4*>(a.part_o) + blk * (R::GPL / 2) * 64 + lane;
+#pragma unroll
+    for (int k = 0; k < R::GPL / 2; ++k) {
+      const int dt = k / 2, q0 = 8 * (k % 2);  // groups 2k, 2k+1: oacc[dt][q0 .. q0+8)
+      u32x4 h;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) h[e] = pack_f16x2(oacc[dt][q0 + 2 * e] * mul, oacc[dt][q0 + 2 * e + 1] * mul);
+      po[k * 64] = h;
     }
-    if (u == 0) {
-      a.part_ml[prow * 2] = m_run;
-      a.part_ml[prow * 2 + 1] = l_tot;
-    }
+    if (u == 0)
+      *reinterpret_cast<f32x4*>(a.part_ml + (((size_t)s * a.Hkv + g) * a.Mpad + row) * 4) =
+          f32x4{m_run, l_tot, __builtin_amdgcn_ldexpf(1.f, ex), 0.f};
   }
 }
 
 // Merge the splits of each query row:
-// O = sum_s 2^(m_s - m) O_s / sum_s 2^(m_s - m) l_s with m = max_s m_s.
-// A split that saw no allowed key has m_s = -inf, l_s = 0 and O_s = 0 and
-// gets weight zero.  Every load is issued before any arithmetic (one round
-// trip to memory): splits past the count re-read the last split and get
-// weight zero.
+// O = sum_s 2^(m_s - m) l_s c_s P_s / sum_s 2^(m_s - m) l_s with m = max_s
+// m_s, where P_s is the stored fp16 partial and c_s its scale.  A split
+// that saw no allowed key has m_s = -inf and l_s = 0 and gets weight zero.
+// One wave per (KV head, 32-row block, pair of O^T groups): lane (c, u)
+// owns row c and the 8 columns 32(k/2) + 16(k%2) + 4u + {0..3, 8..11}.
+// Every load is issued before any arithmetic (one round trip to memory):
+// splits past the count re-read the last split and get weight zero.
 template <int D, int SMAX>
 __global__ __launch_bounds__(256) void tree_attn_combine_kernel(AttnArgs a) {
-  constexpr int TPR = D / 4;  // threads per row, 4 columns each
-  const int gr = blockIdx.x * (256 / TPR) + threadIdx.x / TPR;
-  if (gr >= a.Hkv * a.M) return;
-  const int g = gr / a.M, r = gr % a.M;
-  const int d0 = (threadIdx.x % TPR) * 4;
-  const size_t stride = (size_t)a.Hkv * a.Mpad;  // rows between consecutive splits
-  const size_t row0 = (size_t)g * a.Mpad + r;
-  f32x2_t ml[SMAX];
-  f32x4 o[SMAX];
+  constexpr int NP = D / 16;  // group pairs per lane
+  const int lane = threadIdx.x & 63;
+  const int wv = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int nblk = a.Mpad / 32;
+  if (wv >= a.Hkv * nblk * NP) return;
+  const int k = wv % NP, blk = (wv / NP) % nblk, g = wv / (NP * nblk);
+  const int c = lane & 31, u = lane >> 5;
+  const int r = blk * 32 + c;
+  if (r >= a.M) return;
+  const size_t split_o = (size_t)a.Hkv * nblk * NP * 64;  // 16-byte units between consecutive splits
+  const size_t split_ml = (size_t)a.Hkv * a.Mpad;         // rows between consecutive splits
+  const u32x4* po = reinterpret_cast<const u32x4*>(a.part_o) + (((size_t)g * nblk + blk) * NP + k) * 64 + lane;
+  const f32x4* pml = reinterpret_cast<const f32x4*>(a.part_ml) + (size_t)g * a.Mpad + r;
+  f32x4 ml[SMAX];
+  u32x4 o[SMAX];
 #pragma unroll
   for (int s = 0; s < SMAX; ++s) {
-    const size_t prow = row0 + (size_t)min(s, a.splits - 1) * stride;
-    ml[s] = *reinterpret_cast<const f32x2_t*>(a.part_ml + prow * 2);
-    o[s] = *reinterpret_cast<const f32x4*>(a.part_o + prow * D + d0);
+    const int sc = min(s, a.splits - 1);
+    ml[s] = pml[sc * split_ml];
+    o[s] = po[sc * split_o];
   }
   float m = -INFINITY;
 #pragma unroll
   for (int s = 0; s < SMAX; ++s) m = __builtin_fmaxf(m, ml[s][0]);
   const float base = m == -INFINITY ? 0.f : m;
   float den = 0.f;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int s = 0; s < SMAX; ++s) {
-    const float wgt = s < a.splits ? __builtin_amdgcn_exp2f(ml[s][0] - base) : 0.f;
-    den += wgt * ml[s][1];
-    acc += wgt * o[s];
+    const float wgt = s < a.splits ? __builtin_amdgcn_exp2f(ml[s][0] - base) * ml[s][1] : 0.f;
+    den += wgt;
+    const float wv2 = wgt * ml[s][2];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const f32x2_t h = unpack_f16x2(o[s][e]);
+      acc[2 * e] += wv2 * h[0];
+      acc[2 * e + 1] += wv2 * h[1];
+    }
   }
   const float inv = 1.f / den;
   const int node = r / a.G, head = g * a.G + r % a.G;
-  u32x2 pk;
-  pk[0] = pack_bf16x2(acc[0] * inv, acc[1] * inv);
-  pk[1] = pack_bf16x2(acc[2] * inv, acc[3] * inv);
-  *reinterpret_cast<u32x2*>(a.out + ((size_t)node * a.Hq + head) * D + d0) = pk;
+  uint16_t* orow = a.out + ((size_t)node * a.Hq + head) * D + 32 * (k / 2) + 16 * (k % 2) + 4 * u;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    u32x2 pk;
+    pk[0] = pack_bf16x2(acc[4 * h] * inv, acc[4 * h + 1] * inv);
+    pk[1] = pack_bf16x2(acc[4 * h + 2] * inv, acc[4 * h + 3] * inv);
+    *reinterpret_cast<u32x2*>(orow + 8 * h) = pk;
+  }
 }
 
 // float32 path: one wave per (node, query head), keys walked in order with
@@ -646,8 +681,7 @@ Plan make_plan(int N, int Hq, int Hkv, int D, int P, ooo_dtype dt) {
   if (splits < 1) splits = 1;
   p.splits = splits;
   if (splits > 1)
-    p.ws_bytes = (size_t)splits * Hkv * p.Mpad * (size_t)D * sizeof(float) +
-                 (size_t)splits * Hkv * p.Mpad * 2 * sizeof(float) + 256;
+    p.ws_bytes = (size_t)splits * Hkv * p.Mpad * (size_t)D * 2 + (size_t)splits * Hkv * p.Mpad * 16 + 256;
   return p;
 }
 
@@ -720,8 +754,8 @@ extern "C" int ooo_tree_attn(const void* q, const void* k_cache, const void* v_c
     a.tiles_prefix = p.tiles_prefix;
     a.tiles_total = p.tiles_total;
     if (p.splits > 1) {
-      a.part_o = (float*)workspace;
-      a.part_ml = a.part_o + (size_t)p.splits * n_kv_heads * p.Mpad * head_dim;
+      a.part_o = (uint32_t*)workspace;
+      a.part_ml = (float*)((uint8_t*)workspace + (size_t)p.splits * n_kv_heads * p.Mpad * head_dim * 2);
     }
     const dim3 grid(n_kv_heads * p.row_blocks * p.splits);
     if (head_dim == 128) {
@@ -732,9 +766,8 @@ extern "C" int ooo_tree_attn(const void* q, const void* k_cache, const void* v_c
       else tree_attn_bf16_kernel<64, 4, false><<<grid, 256, 0, st>>>(a);
     }
     if (p.splits > 1) {
-      const int rows = n_kv_heads * a.M;
-      const int rows_per_block = 256 / (head_dim / 4);
-      const dim3 cgrid((rows + rows_per_block - 1) / rows_per_block);
+      const int waves = n_kv_heads * (p.Mpad / 32) * (head_dim / 16);
+      const dim3 cgrid((waves + 3) / 4);
       if (head_dim == 128) {
         if (p.splits <= 8) tree_attn_combine_kernel<128, 8><<<cgrid, 256, 0, st>>>(a);
         else if (p.splits <= 16) tree_attn_combine_kernel<128, 16><<<cgrid, 256, 0, st>>>(a);
