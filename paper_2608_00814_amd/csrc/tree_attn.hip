@@ -412,9 +412,9 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
       for (int hf = 0; hf < NH; ++hf) snxt[hf] = f32x16{};
       qk_mfma(0, kf, snxt);
       float ps = probs_half(scur[0], m_use, pf[0], pf[1]);
-      kread(sb, 1, kf);
+      if (D / 64 > 1) kread(sb, 1, kf);
       __builtin_amdgcn_sched_barrier(0);
-      qk_mfma(1, kf, snxt);
+      if (D / 64 > 1) qk_mfma(1, kf, snxt);
       if (NH == 2) ps += probs_half(scur[NH - 1], m_use, pf[2 * NH - 2], pf[2 * NH - 1]);
       vread(sa, 1, vv1);
       l_run += ps;

@@ -66,7 +66,7 @@ class VerifyRunner:
         self.bonus = self.res[1:2]
         self.path = self.res[2:]
         self.h_res = torch.zeros_like(self.res, device="cpu").pin_memory()
-        self.attn_ws = torch.empty(64, dtype=torch.float32, device=dev)
+        self.attn_ws = torch.zeros(64, dtype=torch.float32, device=dev)
         for nn in sorted({1, max(1, max_nodes // 2), max_nodes}):
             self.ensure_workspace(max(max_prefix, 1), nn)
         lws = ooo.lmhead_workspace(max_nodes, hidden, vocab, self.code)
@@ -95,7 +95,7 @@ class VerifyRunner:
         n = self.n_nodes if n_nodes is None else n_nodes
         need = ooo.tree_attn_workspace(max(n, 1), self.Hq, self.Hkv, self.D, prefix_len, self.code)
         if need > self.attn_ws.numel() * 4:
-            self.attn_ws = torch.empty(need // 4 + 1, dtype=torch.float32, device=self.device)
+            self.attn_ws = torch.zeros(need // 4 + 1, dtype=torch.float32, device=self.device)  # counters start at 0
 
     # -- device -------------------------------------------------------------
     def upload_tree(self, stream=None) -> None:

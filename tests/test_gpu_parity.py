@@ -120,7 +120,7 @@ def _run_attn(q, k, v, P, N, mask, Hq, Hkv, D, dt):
     md = torch.from_numpy(mask.view(np.int64)).to(DEV)
     out = torch.full((N, Hq, D), float("nan"), dtype=tdt, device=DEV)
     ws_n = ooo.tree_attn_workspace(N, Hq, Hkv, D, P, code)
-    ws = torch.empty(max(ws_n, 4) // 4 + 1, dtype=torch.float32, device=DEV)
+    ws = torch.zeros(max(ws_n, 4) // 4 + 1, dtype=torch.float32, device=DEV)  # split counters start at 0
     ooo.tree_attn(qd, kd, vd, P, N, md, Hq, Hkv, 1.0 / math.sqrt(D), out, ws)
     torch.cuda.synchronize()
     return gh.wl.to_f64(gh.to_host(out, dt), dt)
@@ -156,6 +156,29 @@ def test_attention_split_counts_agree(splits, monkeypatch):
     assert np.array_equal(a, b)
     ref = ov.tree_attention(wl.to_f64(q, "bf16"), wl.to_f64(k, "bf16"), wl.to_f64(v, "bf16"), P, t["parent"], Hkv)
     assert gh.row_rel_err(a, ref) <= gh.ATTN_TOL
+
+
+def test_attention_workspace_reuse_across_shapes(monkeypatch):
+    """One workspace serves calls of different shapes, head sizes and split
+    counts in a row: nothing a call reads from it is left over from another."""
+    print("case attention workspace reuse", flush=True)
+    shapes = [(1500, 64, 4, 2, 128, "16"), (300, 33, 2, 3, 64, "5"), (4096, 64, 4, 8, 128, "16"), (700, 100, 4, 1, 128, "7")]
+    need = max(ooo.tree_attn_workspace(N, G * Hkv, Hkv, D, P, ooo.BF16) for P, N, G, Hkv, D, _ in shapes)
+    ws = torch.full((need // 4 + 1,), float("nan"), dtype=torch.float32, device=DEV)
+    for P, N, G, Hkv, D, splits in shapes:
+        monkeypatch.setenv("OOO_ATTN_SPLITS", splits)
+        rs, q, k, v, cap = _attn_inputs(P, N, G, Hkv, D, "bf16", seed=P + N)
+        t = _trie("random", N, rs)
+        W = (N + 63) // 64
+        mask = ov.ancestor_masks(t["parent"], W)
+        qd, kd, vd = gh.to_dev(q, "bf16", DEV), gh.to_dev(k, "bf16", DEV), gh.to_dev(v, "bf16", DEV)
+        md = torch.from_numpy(mask.view(np.int64)).to(DEV)
+        out = torch.full((N, G * Hkv, D), float("nan"), dtype=torch.bfloat16, device=DEV)
+        ooo.tree_attn(qd, kd, vd, P, N, md, G * Hkv, Hkv, 1.0 / math.sqrt(D), out, ws)
+        torch.cuda.synchronize()
+        got = gh.wl.to_f64(gh.to_host(out, "bf16"), "bf16")
+        ref = ov.tree_attention(wl.to_f64(q, "bf16"), wl.to_f64(k, "bf16"), wl.to_f64(v, "bf16"), P, t["parent"], Hkv)
+        assert gh.row_rel_err(got, ref) <= gh.ATTN_TOL
 
 
 def test_attention_ignores_rows_outside_prefix_and_tree():
