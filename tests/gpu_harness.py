@@ -173,3 +173,121 @@ def run_and_check(name: str, seed: int = 0, layers: Optional[Sequence[int]] = No
         assert np.array_equal(kg, kr) and np.array_equal(vg, vr), f"compaction differs in layer {l}"
     log(f"[{name}] all checks passed ({time.time() - t0:.1f}s)", verbose)
     return out
+
+
+def _par(fn, items):
+    """Map fn over items on a thread pool (numpy releases the GIL while it draws)."""
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(8) as ex:
+        return list(ex.map(fn, items))
+
+
+def run_decode(name: str = "llama3.1-8b-decode", seed: int = 0, steps: Optional[int] = None,
+               attn_steps: Sequence[int] = (0, 29, 30, 199), attn_layers: Sequence[int] = (0, 15, 31),
+               sample_rows: int = 6, verbose: bool = False) -> Dict:
+    """Consecutive verification steps with compaction, each step's root the
+    previous step's bonus token and the prefix growing by L+1.  Every step:
+    the trie matches the reference packing, the greedy token of every node
+    is the designated one (planted by construction), and L, path and bonus
+    match the reference walk.  At ``attn_steps``: the LM head against the
+    reference logits and sampled attention rows of ``attn_layers`` against
+    the reference, with the committed prefix rebuilt from generator rows.
+    At the end: the committed cache rows of ``attn_layers`` equal the
+    prefix followed by the accepted nodes' rows, bit for bit."""
+    t0 = time.time()
+    cfg = wl.CONFIGS[name]
+    dt = cfg.dtype
+    steps = cfg.steps if steps is None else steps
+    dev = torch.device("cuda:0")
+    tdt = torch_dtype(dt)
+    P = cfg.prefix_len
+    runner = VerifyRunner(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.hidden, cfg.vocab,
+                          cfg.max_nodes, cfg.max_depth, tdt, dev, max_prefix=cfg.cap - cfg.max_nodes)
+    w = wl.lm_head_weight(cfg, seed)
+    runner.set_weight(to_dev(w, dt, dev))
+    shp = (cfg.n_layers, cfg.n_kv_heads, cfg.cap, cfg.head_dim)
+    k_dev = torch.zeros(shp, dtype=tdt, device=dev)
+    v_dev = torch.zeros(shp, dtype=tdt, device=dev)
+    exp_k: Dict[int, np.ndarray] = {}
+    exp_v: Dict[int, np.ndarray] = {}
+
+    def load_prefix(l):
+        return l, wl.prefix_kv(cfg, seed, l)
+
+    for l, (kp, vp) in _par(load_prefix, range(cfg.n_layers)):
+        k_dev[l, :, :P].copy_(to_dev(kp, dt, dev))
+        v_dev[l, :, :P].copy_(to_dev(vp, dt, dev))
+        if l in attn_layers:
+            exp_k[l] = np.zeros(shp[1:], dtype=kp.dtype)
+            exp_v[l] = np.zeros(shp[1:], dtype=vp.dtype)
+            exp_k[l][:, :P] = kp
+            exp_v[l][:, :P] = vp
+    torch.cuda.synchronize()
+    log(f"[{name}] prefix of {P} rows uploaded ({time.time() - t0:.1f}s)", verbose)
+
+    root = None
+    total_tokens = 0
+    worst_attn = worst_logit = 0.0
+    rs = np.random.default_rng(seed + 2000)
+    for step in range(steps):
+        cands = wl.candidates_for(cfg, seed, step, root_token=root)
+        tree = ov.pack_tree(cands.root_token, cands.seqs, cands.max_nodes, cands.max_depth)
+        N = tree["n_nodes"]
+        toks, offs = cands.csr()
+        packed = runner.pack(cands.root_token, toks, offs)
+        assert packed["n_nodes"] == N and packed["n_truncated"] == tree["n_truncated"], step
+        assert np.array_equal(packed["token"], tree["token"]) and np.array_equal(packed["parent"], tree["parent"])
+        tau, planted = wl.designated_tokens(cfg, seed, step, cands, tree["token"], tree["parent"])
+        acc = ov.accept_walk(tree["token"], tree["parent"], tau)
+        assert acc["L"] == planted, (step, acc["L"], planted)
+        x = wl.hidden_rows(cfg, seed, step, w, tau, N)
+        qs = _par(lambda l: wl.queries(cfg, seed, step, l, N), range(cfg.n_layers))
+        kvs = _par(lambda l: wl.tree_kv(cfg, seed, step, l, N), range(cfg.n_layers))
+        for l in range(cfg.n_layers):
+            k_dev[l, :, P:P + N].copy_(to_dev(kvs[l][0], dt, dev))
+            v_dev[l, :, P:P + N].copy_(to_dev(kvs[l][1], dt, dev))
+        q_dev = [to_dev(q, dt, dev) for q in qs]
+        check_now = step in attn_steps
+        logits_dev = torch.empty(N, cfg.vocab, dtype=torch.float32, device=dev) if check_now else None
+        runner.ensure_workspace(P)
+        runner.device_step(q_dev, k_dev, v_dev, to_dev(x, dt, dev), P, logits=logits_dev, compact=True)
+        torch.cuda.synchronize()
+        res = runner.result()
+        ids = runner.ids[:N].cpu().numpy()
+        assert np.array_equal(ids, tau.astype(np.int32)), f"step {step}: greedy tokens differ from the planted ones"
+        assert res.L == acc["L"] and res.bonus == acc["bonus"], (step, res.L, acc["L"], res.bonus, acc["bonus"])
+        assert np.array_equal(res.path, acc["path"]), step
+        if check_now:
+            ref_logits = ov.lm_head_logits(wl.to_f64(x, dt), wl.to_f32(w, dt))
+            g = ov.greedy_tokens(ref_logits)
+            assert g["margin"].min() >= MIN_MARGIN and np.array_equal(g["ids"], ids), step
+            worst_logit = max(worst_logit, row_rel_err(logits_dev.cpu().numpy(), ref_logits))
+            assert worst_logit <= LOGIT_TOL, (step, worst_logit)
+            for l in attn_layers:
+                k64 = wl.to_f64(exp_k[l][:, :P + N], dt)
+                v64 = wl.to_f64(exp_v[l][:, :P + N], dt)
+                k64[:, P:P + N] = wl.to_f64(kvs[l][0], dt)
+                v64[:, P:P + N] = wl.to_f64(kvs[l][1], dt)
+                q64 = wl.to_f64(qs[l], dt)
+                got = wl.to_f64(to_host(runner.out[l, :N], dt), dt)
+                for _ in range(sample_rows):
+                    i, h = int(rs.integers(0, N)), int(rs.integers(0, cfg.n_q_heads))
+                    ref = ov.attention_row(q64, k64, v64, P, tree["parent"], cfg.n_kv_heads, i, h)
+                    e = row_rel_err(got[i, h][None], ref[None])
+                    worst_attn = max(worst_attn, e)
+                    assert e <= ATTN_TOL, (step, l, i, h, e)
+            log(f"[{name}] step {step}: P={P} N={N} L={res.L} checked ({time.time() - t0:.1f}s)", verbose)
+        # expected committed rows: accepted node at depth d lands in row P + d
+        for l in attn_layers:
+            for d, node in enumerate(acc["path"]):
+                exp_k[l][:, P + d] = kvs[l][0][:, node]
+                exp_v[l][:, P + d] = kvs[l][1][:, node]
+        P += res.L + 1
+        total_tokens += res.L + 1
+        root = res.bonus
+    for l in attn_layers:
+        assert np.array_equal(to_host(k_dev[l, :, :P], dt), exp_k[l][:, :P]), f"committed K rows differ, layer {l}"
+        assert np.array_equal(to_host(v_dev[l, :, :P], dt), exp_v[l][:, :P]), f"committed V rows differ, layer {l}"
+    log(f"[{name}] {steps} steps, {total_tokens} tokens committed, final P={P} ({time.time() - t0:.1f}s)", verbose)
+    return {"steps": steps, "tokens": total_tokens, "final_prefix": P, "attn_rel": worst_attn,
+            "logit_rel": worst_logit}

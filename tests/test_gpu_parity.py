@@ -57,6 +57,14 @@ def test_step_qwen3_8b_second_seed_sampled():
     gh.run_and_check("qwen3-8b", seed=1, layers=[0, 35], sample_rows=4, verbose=True)
 
 
+def test_decode_llama31_8b_200_steps():
+    """Llama-3.1-8B shape: 200 consecutive verify steps with compaction from a
+    32768-row prefix (256-node tries, a hint branch from step 30)."""
+    print("case decode llama3.1-8b 200 steps", flush=True)
+    r = gh.run_decode("llama3.1-8b-decode", seed=0, verbose=True)
+    assert r["steps"] == 200 and r["final_prefix"] == 32768 + r["tokens"]
+
+
 def test_step_qwen25_32b_sampled():
     print("case qwen2.5-32b seed=0 (layers 0, 63 full; sampled rows elsewhere)", flush=True)
     gh.run_and_check("qwen2.5-32b", seed=0, layers=[0, 63], sample_rows=4, verbose=True)
