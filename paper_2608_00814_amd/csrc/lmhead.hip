@@ -295,25 +295,12 @@ struct LmPlan {
   size_t ws_bytes;
 };
 
-// Blocks of the persistent bf16 grid: one per compute unit of the device.
-int device_cus() {
-  static int cached[64] = {0};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cached[dev] == 0) {
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-    cached[dev] = n;
-  }
-  return cached[dev];
-}
-
 LmPlan lm_plan(int N, int H, int V, ooo_dtype dt) {
   LmPlan p{};
   if (dt == OOO_BF16) {
     p.nb = N <= 32 ? 1 : N <= 64 ? 2 : N <= 128 ? 4 : 8;
     const int tiles = (V + kLmRows - 1) / kLmRows;
-    p.blocks = tiles < device_cus() ? tiles : device_cus();
+    p.blocks = tiles < device_cus() ? tiles : device_cus();  // persistent grid: one block per CU
   } else {
     p.blocks = (V + 255) / 256;
   }

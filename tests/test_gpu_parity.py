@@ -171,7 +171,10 @@ def test_attention_workspace_reuse_across_shapes(monkeypatch):
     counts in a row: nothing a call reads from it is left over from another."""
     print("case attention workspace reuse", flush=True)
     shapes = [(1500, 64, 4, 2, 128, "16"), (300, 33, 2, 3, 64, "5"), (4096, 64, 4, 8, 128, "16"), (700, 100, 4, 1, 128, "7")]
-    need = max(ooo.tree_attn_workspace(N, G * Hkv, Hkv, D, P, ooo.BF16) for P, N, G, Hkv, D, _ in shapes)
+    need = 0
+    for P, N, G, Hkv, D, splits in shapes:
+        monkeypatch.setenv("OOO_ATTN_SPLITS", splits)
+        need = max(need, ooo.tree_attn_workspace(N, G * Hkv, Hkv, D, P, ooo.BF16))
     ws = torch.full((need // 4 + 1,), float("nan"), dtype=torch.float32, device=DEV)
     for P, N, G, Hkv, D, splits in shapes:
         monkeypatch.setenv("OOO_ATTN_SPLITS", splits)
