@@ -58,6 +58,10 @@ __device__ __forceinline__ int sigma(int c) { return (c & ~0xC) | ((c & 4) << 1)
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 #define OOO_LDS(p) ((__attribute__((address_space(3))) void*)(p))
 #define OOO_GLB(p) ((const __attribute__((address_space(1))) void*)(p))
+// Kernel-local lambdas must be inlined: an outlined call would take its
+// captures through memory and lose their wave-uniformity (the DMA needs
+// scalar operands).
+#define OOO_INLINE __attribute__((always_inline))
 
 // Workgroup barrier without the memory-model fence __syncthreads() adds: the
 // fence would make the loader wave wait for every in-flight LDS DMA.  The
@@ -72,6 +76,12 @@ __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "mem
 // barrier).  M0 holds the LDS base; nothing else in these kernels uses M0.
 __device__ __forceinline__ void dma16(const void* base, uint32_t voff, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(base)
+               : "memory", "m0");
+}
+
+// Same for 4 bytes per lane (lane l's dword lands at lds + 4*l).
+__device__ __forceinline__ void dma4(const void* base, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, %2" ::"s"(lds), "v"(voff), "s"(base)
                : "memory", "m0");
 }
 
@@ -168,6 +178,7 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
   const int ntiles = t_end - t_begin;  // >= 1 because splits <= tiles
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t wave_u = __builtin_amdgcn_readfirstlane(wave);
   const int rg = wave % RG, kh0 = SPLIT ? wave / RG : 0;
   const int c = lane & 31, u = lane >> 5;
   uint64_t* const mrow = mwords + (rg * 32 + c) * kMaxMaskWords;
@@ -179,15 +190,16 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
   const uint16_t* const kg = a.k + (size_t)g * a.cap * D;
   const uint16_t* const vg = a.v + (size_t)g * a.cap * D;
 
-  // Q^T fragments (B operand of S^T = K Q^T): row c, k = 16dk + 8u .. +8
+  // Q^T fragments (B operand of S^T = K Q^T): row c, k = 16dk + 8u .. +8.
+  // The key-split kernel stages Q through LDS instead (below).
   bf16x8 qf[D / 16];
-  {
+  if constexpr (!SPLIT) {
     const uint16_t* qrow = a.q + ((size_t)node * a.Hq + head) * D;
 #pragma unroll
     for (int dk = 0; dk < D / 16; ++dk) qf[dk] = as_bf16x8(ld16(qrow + 16 * dk + 8 * u));
   }
 
-  auto tile_rows = [&](int t, int& row0, int& limit) {
+  auto tile_rows = [&](int t, int& row0, int& limit) OOO_INLINE {
     if (t < a.tiles_prefix) {
       row0 = t * kTile;
       limit = a.P;
@@ -202,14 +214,13 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
   // below from a uniform tile base; a tile that crosses the end of its
   // region clamps rows past it to the last valid row (masked keys, zero
   // probability).
-  const uint32_t wave_u = __builtin_amdgcn_readfirstlane(wave);
   uint32_t dvoff[PM];
 #pragma unroll
   for (int i = 0; i < PM; ++i) {
     const int r = (i * NW + wave) * R::RPI + lane / R::CH;
     dvoff[i] = r * R::ROWB + R::swz(r, lane % R::CH) * 16;
   }
-  auto issue = [&](int t, auto stage_c) {
+  auto issue = [&](int t, auto stage_c) OOO_INLINE {
     constexpr int ST = decltype(stage_c)::value;
     int row0, limit;
     tile_rows(t, row0, limit);
@@ -235,8 +246,36 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
 
   // The mask words go through LDS so that no global load is pending inside
   // the tile loop, where a wait for it would also wait for the tile DMA.
-  if (kh0 == 0)
+  if constexpr (!SPLIT) {
     for (int wd = u; wd < a.W; wd += 2) mrow[wd] = a.mask[(size_t)node * a.W + wd];
+  } else {
+    // Key-split kernel: Q and the mask words arrive by DMA as well, so the
+    // kernel has no compiler-tracked load at all (the compiler would wait
+    // for one with vmcnt(0), which also waits for every tile in flight).
+    // Q rows of the block, row-major with the K chunk permutation, go to
+    // ring stage 3 (rows 0..63 in k3, 64..127 in v3): tile 3 is not
+    // requested before every wave has read its fragments.  Mask words go
+    // to mwords as [row][W] (dword DMA, 64 dwords per instruction).
+    const auto row_src = [&](int r) OOO_INLINE {
+      const int rq = min(rb * BM + r, a.M - 1);
+      return rq / a.G;
+    };
+    for (int j = wave_u; j < BM / R::RPI; j += NW) {
+      const int r = j * R::RPI + lane / R::CH;
+      const int rq = min(rb * BM + r, a.M - 1);
+      const int nd = rq / a.G;
+      const uint32_t off = (uint32_t)((nd * a.Hq + g * a.G + (rq - nd * a.G)) * D) * 2u +
+                           (uint32_t)R::swz(r, lane % R::CH) * 16u;
+      const uint32_t dst = j * R::RPI < 64 ? lds_addr(k3) + j * 1024 : lds_addr(v3) + (j - 64 / R::RPI) * 1024;
+      dma16(a.q, off, dst);
+    }
+    const int nmask = BM * 2 * a.W / 64;  // dword instructions
+    for (int j = wave_u; j < nmask; j += NW) {
+      const int e = j * 64 + lane;
+      const int r = e / (2 * a.W), k = e - r * (2 * a.W);
+      dma4(a.mask, (uint32_t)(row_src(r) * 2 * a.W + k) * 4u, lds_addr(mwords) + j * 256);
+    }
+  }
 
   // Only the first tile is requested up front: when every block asks for
   // several tiles at once, each block's first tile lands late.
@@ -269,7 +308,7 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
   float m_run = -INFINITY, l_run = 0.f;
 
   // K fragments of k-steps 4b .. 4b+3 for the wave's halves
-  auto kread = [&](auto stage_c, int b, bf16x8 (&kf)[NH][4]) {
+  auto kread = [&](auto stage_c, int b, bf16x8 (&kf)[NH][4]) OOO_INLINE {
     constexpr int ST = decltype(stage_c)::value;
     const uint8_t* Ks = kst[ST];
 #pragma unroll
@@ -278,14 +317,14 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
       for (int hf = 0; hf < NH; ++hf)
         kf[hf][j] = as_bf16x8(*reinterpret_cast<const u32x4*>(Ks + koff[4 * b + j] + 32 * hf * R::ROWB));
   };
-  auto qk_mfma = [&](int b, const bf16x8 (&kf)[NH][4], f32x16 (&acc)[NH]) {
+  auto qk_mfma = [&](int b, const bf16x8 (&kf)[NH][4], f32x16 (&acc)[NH]) OOO_INLINE {
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int hf = 0; hf < NH; ++hf) acc[hf] = mfma32(kf[hf][j], qf[4 * b + j], acc[hf]);
   };
   // V^T fragments of local key step ks (16 keys of the wave's range)
-  auto vread = [&](auto stage_c, int ks, bf16x8 (&vv)[D / 32]) {
+  auto vread = [&](auto stage_c, int ks, bf16x8 (&vv)[D / 32]) OOO_INLINE {
     constexpr int ST = decltype(stage_c)::value;
     const uint8_t* Vs = vst[ST];
 #pragma unroll
@@ -300,12 +339,12 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
       vv[dt] = as_bf16x8(u32x4{lohi[0][0], lohi[0][1], lohi[1][0], lohi[1][1]});
     }
   };
-  auto pv_mfma = [&](const bf16x8 (&vv)[D / 32], const bf16x8& p) {
+  auto pv_mfma = [&](const bf16x8 (&vv)[D / 32], const bf16x8& p) OOO_INLINE {
 #pragma unroll
     for (int dt = 0; dt < D / 32; ++dt) oacc[dt] = mfma32(vv[dt], p, oacc[dt]);
   };
   // probabilities of one 32-key half in B-operand order; returns their sum
-  auto probs_half = [&](const f32x16& acc, float m_use, bf16x8& p0, bf16x8& p1) {
+  auto probs_half = [&](const f32x16& acc, float m_use, bf16x8& p0, bf16x8& p1) OOO_INLINE {
     float psum = 0.f;
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) {
@@ -324,12 +363,13 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
   };
   // Mask tile t's scores (tree tiles and ragged tails only).  Lane value j
   // of half hf is key 32(kh0+hf) + 16*(j/8) + 8u + j%8 of the tile.
-  auto apply_mask = [&](int t, f32x16 (&acc)[NH]) {
+  auto apply_mask = [&](int t, f32x16 (&acc)[NH]) OOO_INLINE {
     int row0, limit;
     tile_rows(t, row0, limit);
     const bool tree = t >= a.tiles_prefix;
     if (tree || row0 + kTile > limit) {
-      const uint64_t mw = tree ? mrow[t - a.tiles_prefix] : ~0ull;
+      const uint64_t mw =
+          !tree ? ~0ull : SPLIT ? mwords[(rg * 32 + c) * a.W + (t - a.tiles_prefix)] : mrow[t - a.tiles_prefix];
 #pragma unroll
       for (int hf = 0; hf < NH; ++hf)
 #pragma unroll
@@ -341,7 +381,7 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
     }
   };
   // row max of a tile's scores over the wave's keys, in log2 units
-  auto row_max = [&](const f32x16 (&acc)[NH]) {
+  auto row_max = [&](const f32x16 (&acc)[NH]) OOO_INLINE {
     float mh[NH];
 #pragma unroll
     for (int hf = 0; hf < NH; ++hf) {
@@ -357,7 +397,7 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
   // Lazy rescaling: the reference max m_run moves only when some row of the
   // wave grows by more than 2^8, so probabilities stay <= 256 (fine for fp32
   // sums and bf16 operands) and O, l are rescaled rarely.
-  auto rescale = [&](float mx) {
+  auto rescale = [&](float mx) OOO_INLINE {
     if (__any(mx > m_run + 8.f)) {
       const float m_new = __builtin_fmaxf(m_run, mx);
       const float alpha = __builtin_amdgcn_exp2f(m_run - (m_new == -INFINITY ? 0.f : m_new));
@@ -368,117 +408,196 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
     }
   };
 
-  // prologue: scores, mask and max of the first tile
-  f32x16 sa_buf[NH], sb_buf[NH];
-  wait_vmcnt<0>();
-  wg_barrier();
-  if (ntiles > 1) issue(t_begin + 1, std::integral_constant<int, 1>{});
-  if (ntiles > 2) issue(t_begin + 2, std::integral_constant<int, 2>{});
-  {
-    bf16x8 kf[NH][4];
+  if constexpr (SPLIT) {
+    // Two waves per SIMD, one per key half of the same rows, half a tile
+    // apart: wave A (kh0 = 0) runs scores, softmax and P V of tile i between
+    // barriers i and i+1; wave B runs P V of tile i-1, then scores and
+    // softmax of tile i.  So while one wave is in its softmax (vector
+    // units) the other issues matrix-core work.  Because B reads V of tile
+    // i-1 after barrier i, the ring runs two tiles ahead: barrier i is
+    // followed by the DMA of tile i+2 into the stage of tile i-2.
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    using I3 = std::integral_constant<int, 3>;
+    if (ntiles > 1) issue(t_begin + 1, I1{});
+    // Tile 0 landed (the compiler does not track the DMA, so the barrier
+    // alone would not wait for it); the mask words in LDS are visible.
+    wait_tiles<PER, 1>(min(1, ntiles - 1));
+    __syncthreads();
+    {
+      const int rq = rg * 32 + c;
+      const uint8_t* qs = (rg < 2 ? k3 : v3) + (rq % 64) * R::ROWB;
 #pragma unroll
-    for (int hf = 0; hf < NH; ++hf) sa_buf[hf] = f32x16{};
-#pragma unroll
-    for (int b = 0; b < D / 64; ++b) {
-      kread(std::integral_constant<int, 0>{}, b, kf);
-      qk_mfma(b, kf, sa_buf);
+      for (int dk = 0; dk < D / 16; ++dk)
+        qf[dk] = as_bf16x8(*reinterpret_cast<const u32x4*>(qs + (R::swz(rq, 2 * dk + u) << 4)));
     }
-  }
-  apply_mask(t_begin, sa_buf);
-  rescale(row_max(sa_buf));
-
-  // One pipeline step: tile i is in stage SA with its scores in scur, tile
-  // i+1 (if NEXT) in stage SB, its scores go to snxt; tile i+3 is issued
-  // into SD, the stage tile i-1 used.  The row max of tile i+1 is taken
-  // before masking; a masked tile (tree tiles, ragged tails) takes it again
-  // after the mask.  Phases are separated by scheduling barriers.
-  auto step = [&](int i, auto sa, auto sb, auto sd, auto next_c, f32x16 (&scur)[NH], f32x16 (&snxt)[NH]) {
-    constexpr bool NEXT = decltype(next_c)::value;
-    if (NEXT) {
-      wait_tiles<PER, 1>(min(1, ntiles - 2 - i));  // this wave's share of tile i+1 landed
-      wg_barrier();                                // ... and every other wave's
-      if (i + 3 < ntiles) issue(t_begin + i + 3, sd);
-    }
-    const float m_use = m_run == -INFINITY ? 0.f : m_run;
-    bf16x8 pf[2 * NH];
-    bf16x8 vv0[D / 32], vv1[D / 32];
-    if (NEXT) {
-      bf16x8 kf[NH][4];
-      __builtin_amdgcn_sched_barrier(0);
-      kread(sb, 0, kf);
-      vread(sa, 0, vv0);
-      __builtin_amdgcn_sched_barrier(0);
+    if (ntiles > 2) issue(t_begin + 2, I2{});
+    bf16x8 pf_prev[2];  // wave B: probabilities of the previous tile
+    auto pv_tile = [&](auto stage_c, const bf16x8 (&pf)[2]) OOO_INLINE {
 #pragma unroll
-      for (int hf = 0; hf < NH; ++hf) snxt[hf] = f32x16{};
-      qk_mfma(0, kf, snxt);
-      float ps = probs_half(scur[0], m_use, pf[0], pf[1]);
-      if (D / 64 > 1) kread(sb, 1, kf);
-      __builtin_amdgcn_sched_barrier(0);
-      if (D / 64 > 1) qk_mfma(1, kf, snxt);
-      if (NH == 2) ps += probs_half(scur[NH - 1], m_use, pf[2 * NH - 2], pf[2 * NH - 1]);
-      vread(sa, 1, vv1);
-      l_run += ps;
-      __builtin_amdgcn_sched_barrier(0);
-      pv_mfma(vv0, pf[0]);
-      if (NH == 2) vread(sa, 2, vv0);
-      __builtin_amdgcn_sched_barrier(0);
-      pv_mfma(vv1, pf[1]);
-      if (NH == 2) vread(sa, 3, vv1);
-      float mx = row_max(snxt);
-      __builtin_amdgcn_sched_barrier(0);
-      if (NH == 2) {
-        pv_mfma(vv0, pf[2 * NH - 2]);
-        pv_mfma(vv1, pf[2 * NH - 1]);
+      for (int ks = 0; ks < 2; ++ks) {
+        bf16x8 vv[D / 32];
+        vread(stage_c, ks, vv);
+        pv_mfma(vv, pf[ks]);
       }
-      __builtin_amdgcn_sched_barrier(0);
-      int row0, limit;
-      tile_rows(t_begin + i + 1, row0, limit);
-      if (t_begin + i + 1 >= a.tiles_prefix || row0 + kTile > limit) {
-        apply_mask(t_begin + i + 1, snxt);
-        mx = row_max(snxt);
+    };
+    auto body = [&](auto role_c, int i, auto st_c) OOO_INLINE {
+      constexpr bool B = decltype(role_c)::value;
+      constexpr int ST = decltype(st_c)::value;
+      if (i > 0) {
+        wait_tiles<PER, 1>(min(1, ntiles - 1 - i));  // this wave's share of tile i landed
+        wg_barrier();                                // ... and every other wave's
+        if (i + 2 < ntiles) issue(t_begin + i + 2, std::integral_constant<int, (ST + 2) % 4>{});
+        if constexpr (B) pv_tile(std::integral_constant<int, (ST + 3) % 4>{}, pf_prev);
       }
-      rescale(mx);
-    } else {
-      float ps = 0.f;
+      f32x16 sc[1] = {f32x16{}};
+      bf16x8 kf[1][4];
 #pragma unroll
-      for (int hf = 0; hf < NH; ++hf) ps += probs_half(scur[hf], m_use, pf[2 * hf], pf[2 * hf + 1]);
-      l_run += ps;
-#pragma unroll
-      for (int ks = 0; ks < 2 * NH; ++ks) {
-        vread(sa, ks, vv0);
-        pv_mfma(vv0, pf[ks]);
+      for (int b = 0; b < D / 64; ++b) {
+        kread(st_c, b, kf);
+        qk_mfma(b, kf, sc);
       }
-    }
-  };
-  using I0 = std::integral_constant<int, 0>;
-  using I1 = std::integral_constant<int, 1>;
-  using I2 = std::integral_constant<int, 2>;
-  using I3 = std::integral_constant<int, 3>;
-  using YES = std::integral_constant<bool, true>;
-  using NO = std::integral_constant<bool, false>;
-  int i = 0;
-  for (; i + 4 < ntiles; i += 4) {  // steps i .. i+3 all have a next tile
-    step(i, I0{}, I1{}, I3{}, YES{}, sa_buf, sb_buf);
-    step(i + 1, I1{}, I2{}, I0{}, YES{}, sb_buf, sa_buf);
-    step(i + 2, I2{}, I3{}, I1{}, YES{}, sa_buf, sb_buf);
-    step(i + 3, I3{}, I0{}, I2{}, YES{}, sb_buf, sa_buf);
-  }
-  // 1..4 steps remain; the last has no next tile
-  const int rem = ntiles - i;
-  if (rem == 1) {
-    step(i, I0{}, I1{}, I3{}, NO{}, sa_buf, sb_buf);
-  } else if (rem == 2) {
-    step(i, I0{}, I1{}, I3{}, YES{}, sa_buf, sb_buf);
-    step(i + 1, I1{}, I2{}, I0{}, NO{}, sb_buf, sa_buf);
-  } else if (rem == 3) {
-    step(i, I0{}, I1{}, I3{}, YES{}, sa_buf, sb_buf);
-    step(i + 1, I1{}, I2{}, I0{}, YES{}, sb_buf, sa_buf);
-    step(i + 2, I2{}, I3{}, I1{}, NO{}, sa_buf, sb_buf);
+      apply_mask(t_begin + i, sc);
+      rescale(row_max(sc));
+      bf16x8 pf[2];
+      l_run += probs_half(sc[0], m_run == -INFINITY ? 0.f : m_run, pf[0], pf[1]);
+      if constexpr (!B) {
+        pv_tile(st_c, pf);
+      } else {
+        pf_prev[0] = pf[0];
+        pf_prev[1] = pf[1];
+        if (i == ntiles - 1) pv_tile(st_c, pf_prev);
+      }
+    };
+    auto run = [&](auto role_c) OOO_INLINE {
+      int i = 0;
+      for (; i + 4 <= ntiles; i += 4) {
+        body(role_c, i, I0{});
+        body(role_c, i + 1, I1{});
+        body(role_c, i + 2, I2{});
+        body(role_c, i + 3, I3{});
+      }
+      if (i < ntiles) body(role_c, i, I0{});
+      if (i + 1 < ntiles) body(role_c, i + 1, I1{});
+      if (i + 2 < ntiles) body(role_c, i + 2, I2{});
+    };
+    if (__builtin_amdgcn_readfirstlane(kh0) == 0) run(std::false_type{});
+    else run(std::true_type{});
   } else {
-    step(i, I0{}, I1{}, I3{}, YES{}, sa_buf, sb_buf);
-    step(i + 1, I1{}, I2{}, I0{}, YES{}, sb_buf, sa_buf);
-    step(i + 2, I2{}, I3{}, I1{}, YES{}, sa_buf, sb_buf);
-    step(i + 3, I3{}, I0{}, I2{}, NO{}, sb_buf, sa_buf);
+  // prologue: scores, mask and max of the first tile
+    f32x16 sa_buf[NH], sb_buf[NH];
+    wait_vmcnt<0>();
+    wg_barrier();
+    if (ntiles > 1) issue(t_begin + 1, std::integral_constant<int, 1>{});
+    if (ntiles > 2) issue(t_begin + 2, std::integral_constant<int, 2>{});
+    {
+      bf16x8 kf[NH][4];
+#pragma unroll
+      for (int hf = 0; hf < NH; ++hf) sa_buf[hf] = f32x16{};
+#pragma unroll
+      for (int b = 0; b < D / 64; ++b) {
+        kread(std::integral_constant<int, 0>{}, b, kf);
+        qk_mfma(b, kf, sa_buf);
+      }
+    }
+    apply_mask(t_begin, sa_buf);
+    rescale(row_max(sa_buf));
+
+    // One pipeline step: tile i is in stage SA with its scores in scur, tile
+    // i+1 (if NEXT) in stage SB, its scores go to snxt; tile i+3 is issued
+    // into SD, the stage tile i-1 used.  The row max of tile i+1 is taken
+    // before masking; a masked tile (tree tiles, ragged tails) takes it again
+    // after the mask.  Phases are separated by scheduling barriers.
+    auto step = [&](int i, auto sa, auto sb, auto sd, auto next_c, f32x16 (&scur)[NH], f32x16 (&snxt)[NH]) OOO_INLINE {
+      constexpr bool NEXT = decltype(next_c)::value;
+      if (NEXT) {
+        wait_tiles<PER, 1>(min(1, ntiles - 2 - i));  // this wave's share of tile i+1 landed
+        wg_barrier();                                // ... and every other wave's
+        if (i + 3 < ntiles) issue(t_begin + i + 3, sd);
+      }
+      const float m_use = m_run == -INFINITY ? 0.f : m_run;
+      bf16x8 pf[2 * NH];
+      bf16x8 vv0[D / 32], vv1[D / 32];
+      if (NEXT) {
+        bf16x8 kf[NH][4];
+        __builtin_amdgcn_sched_barrier(0);
+        kread(sb, 0, kf);
+        vread(sa, 0, vv0);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int hf = 0; hf < NH; ++hf) snxt[hf] = f32x16{};
+        qk_mfma(0, kf, snxt);
+        float ps = probs_half(scur[0], m_use, pf[0], pf[1]);
+        if (D / 64 > 1) kread(sb, 1, kf);
+        __builtin_amdgcn_sched_barrier(0);
+        if (D / 64 > 1) qk_mfma(1, kf, snxt);
+        if (NH == 2) ps += probs_half(scur[NH - 1], m_use, pf[2 * NH - 2], pf[2 * NH - 1]);
+        vread(sa, 1, vv1);
+        l_run += ps;
+        __builtin_amdgcn_sched_barrier(0);
+        pv_mfma(vv0, pf[0]);
+        if (NH == 2) vread(sa, 2, vv0);
+        __builtin_amdgcn_sched_barrier(0);
+        pv_mfma(vv1, pf[1]);
+        if (NH == 2) vread(sa, 3, vv1);
+        float mx = row_max(snxt);
+        __builtin_amdgcn_sched_barrier(0);
+        if (NH == 2) {
+          pv_mfma(vv0, pf[2 * NH - 2]);
+          pv_mfma(vv1, pf[2 * NH - 1]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        int row0, limit;
+        tile_rows(t_begin + i + 1, row0, limit);
+        if (t_begin + i + 1 >= a.tiles_prefix || row0 + kTile > limit) {
+          apply_mask(t_begin + i + 1, snxt);
+          mx = row_max(snxt);
+        }
+        rescale(mx);
+      } else {
+        float ps = 0.f;
+#pragma unroll
+        for (int hf = 0; hf < NH; ++hf) ps += probs_half(scur[hf], m_use, pf[2 * hf], pf[2 * hf + 1]);
+        l_run += ps;
+#pragma unroll
+        for (int ks = 0; ks < 2 * NH; ++ks) {
+          vread(sa, ks, vv0);
+          pv_mfma(vv0, pf[ks]);
+        }
+      }
+    };
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    using I3 = std::integral_constant<int, 3>;
+    using YES = std::integral_constant<bool, true>;
+    using NO = std::integral_constant<bool, false>;
+    int i = 0;
+    for (; i + 4 < ntiles; i += 4) {  // steps i .. i+3 all have a next tile
+      step(i, I0{}, I1{}, I3{}, YES{}, sa_buf, sb_buf);
+      step(i + 1, I1{}, I2{}, I0{}, YES{}, sb_buf, sa_buf);
+      step(i + 2, I2{}, I3{}, I1{}, YES{}, sa_buf, sb_buf);
+      step(i + 3, I3{}, I0{}, I2{}, YES{}, sb_buf, sa_buf);
+    }
+    // 1..4 steps remain; the last has no next tile
+    const int rem = ntiles - i;
+    if (rem == 1) {
+      step(i, I0{}, I1{}, I3{}, NO{}, sa_buf, sb_buf);
+    } else if (rem == 2) {
+      step(i, I0{}, I1{}, I3{}, YES{}, sa_buf, sb_buf);
+      step(i + 1, I1{}, I2{}, I0{}, NO{}, sb_buf, sa_buf);
+    } else if (rem == 3) {
+      step(i, I0{}, I1{}, I3{}, YES{}, sa_buf, sb_buf);
+      step(i + 1, I1{}, I2{}, I0{}, YES{}, sb_buf, sa_buf);
+      step(i + 2, I2{}, I3{}, I1{}, NO{}, sa_buf, sb_buf);
+    } else {
+      step(i, I0{}, I1{}, I3{}, YES{}, sa_buf, sb_buf);
+      step(i + 1, I1{}, I2{}, I0{}, YES{}, sb_buf, sa_buf);
+      step(i + 2, I2{}, I3{}, I1{}, YES{}, sa_buf, sb_buf);
+      step(i + 3, I3{}, I0{}, I2{}, NO{}, sb_buf, sa_buf);
+    }
+
   }
 
   float l_tot = l_run + shfl_xor_f(l_run, 32);
@@ -723,7 +842,8 @@ extern "C" int ooo_tree_attn(const void* q, const void* k_cache, const void* v_c
   OOO_REQUIRE(dt == OOO_F32 || dt == OOO_BF16, OOO_ERR_INVALID, "ooo_tree_attn: unknown dtype %d", (int)dt);
   OOO_REQUIRE(head_dim == 64 || head_dim == 128, OOO_ERR_UNSUPPORTED,
               "ooo_tree_attn: head_dim %d not supported (64 or 128)", head_dim);
-  OOO_REQUIRE((int64_t)n_nodes * n_q_heads <= (1 << 30), OOO_ERR_UNSUPPORTED, "ooo_tree_attn: too many rows");
+  OOO_REQUIRE((int64_t)n_nodes * n_q_heads * head_dim * 2 < (1LL << 32), OOO_ERR_UNSUPPORTED,
+              "ooo_tree_attn: Q of %d nodes x %d heads exceeds 4 GiB", n_nodes, n_q_heads);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   const int G = n_q_heads / n_kv_heads;
 
@@ -766,7 +886,14 @@ extern "C" int ooo_tree_attn(const void* q, const void* k_cache, const void* v_c
       a.part_ml = (float*)((uint8_t*)workspace + (size_t)p.splits * n_kv_heads * p.Mpad * head_dim * 2);
     }
     const dim3 grid(n_kv_heads * p.row_blocks * p.splits);
-    if (head_dim == 128) {
+    // head_dim 128 runs the key-split kernel (two waves per row group);
+    // OOO_ATTN_SPLITK=0 selects the one-wave pipelined kernel instead.
+    const char* sk_env = getenv("OOO_ATTN_SPLITK");
+    const bool splitk = !sk_env || atoi(sk_env) != 0;
+    if (head_dim == 128 && splitk) {
+      if (p.waves == 2) tree_attn_bf16_kernel<128, 2, true><<<grid, 256, 0, st>>>(a);
+      else tree_attn_bf16_kernel<128, 4, true><<<grid, 512, 0, st>>>(a);
+    } else if (head_dim == 128) {
       if (p.waves == 2) tree_attn_bf16_kernel<128, 2, false><<<grid, 128, 0, st>>>(a);
       else tree_attn_bf16_kernel<128, 4, false><<<grid, 256, 0, st>>>(a);
     } else {

@@ -149,6 +149,26 @@ def test_attention_edges(case):
     assert gh.row_rel_err(got, ref) <= tol
 
 
+ONE_WAVE_CASES = [c for c in ATTN_CASES if c[4] == 128 and c[6] == "bf16"][:6]
+
+
+@pytest.mark.parametrize("case", ONE_WAVE_CASES, ids=[f"P{c[0]}-N{c[1]}-G{c[2]}-Hkv{c[3]}-{c[5]}"
+                                                      for c in ONE_WAVE_CASES])
+def test_attention_one_wave_kernel(case, monkeypatch):
+    """head_dim 128 has two kernels (two waves per row group splitting each
+    key tile, the default, and one wave per row group); both match the
+    oracle."""
+    P, N, G, Hkv, D, kind, dt = case
+    print(f"case attention one-wave kernel {case}", flush=True)
+    monkeypatch.setenv("OOO_ATTN_SPLITK", "0")
+    rs, q, k, v, cap = _attn_inputs(P, N, G, Hkv, D, dt, seed=sum(case[:5]) + 1)
+    t = _trie(kind, N, rs)
+    mask = ov.ancestor_masks(t["parent"], (N + 63) // 64)
+    got = _run_attn(q, k, v, P, N, mask, G * Hkv, Hkv, D, dt)
+    ref = ov.tree_attention(wl.to_f64(q, dt), wl.to_f64(k, dt), wl.to_f64(v, dt), P, t["parent"], Hkv)
+    assert gh.row_rel_err(got, ref) <= gh.ATTN_TOL
+
+
 @pytest.mark.parametrize("splits", ["1", "3", "32"])
 def test_attention_split_counts_agree(splits, monkeypatch):
     """The split-KV decomposition does not change the result beyond rounding,
