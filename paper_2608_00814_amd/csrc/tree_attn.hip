@@ -794,12 +794,12 @@ Plan make_plan(int N, int Hq, int Hkv, int D, int P, ooo_dtype dt) {
   p.tiles_total = p.tiles_prefix + (N + kTile - 1) / kTile;
   // Split count: as many workgroups as fit on the CUs at once, balancing the
   // tiles of the busiest split against the partials every split adds (an
-  // empirical cost of about 1.3 us per 64-key tile and 0.4 us per split).
+  // empirical cost of about 1.3 us per 64-key tile and 0.5 us per split).
   const int base = Hkv * p.row_blocks;
   const int max_splits = device_cus() / base > 1 ? device_cus() / base : 1;
   int splits = 1, best = INT32_MAX;
   for (int sc = 1; sc <= max_splits && sc <= p.tiles_total; ++sc) {
-    const int cost = 13 * ((p.tiles_total + sc - 1) / sc) + 4 * sc;
+    const int cost = 13 * ((p.tiles_total + sc - 1) / sc) + 5 * sc;
     if (cost < best) best = cost, splits = sc;
   }
   if (const char* env = getenv("OOO_ATTN_SPLITS")) splits = atoi(env);
