@@ -15,9 +15,15 @@
 //    softmax state, its probabilities (already in B-operand order for the
 //    second product) and 16 of its output columns, so the online softmax
 //    needs one cross-lane exchange per tile and no LDS round trip.
-//  * V is transposed while it is staged (global -> registers -> LDS).
-//  * Splits write float32 partials (unnormalised O, running max, sum) that
-//    a second kernel combines; with one split the kernel writes O directly.
+//  * K and V tiles stream into a 4-stage LDS ring by DMA (global_load_lds);
+//    the V^T operand is read from the row-major V tile with transposing LDS
+//    reads (ds_read_b64_tr_b16).
+//  * head_dim 128: two waves per 32-row group, each taking one 32-key half
+//    of every tile (two waves per SIMD); head_dim 64: one wave per row group
+//    with a hand-pipelined tile loop.
+//  * Splits write fp16 partials (normalised O times a power of two, plus
+//    max, sum and scale in fp32) that a second kernel combines; with one
+//    split the kernel writes O directly.
 //  * Launch order is XCD-aware: consecutive work items (same KV head and
 //    row block, neighbouring splits) go to blocks that share blockIdx % 8,
 //    so one head's K/V stream stays in one XCD's L2.
@@ -63,9 +69,10 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 // scalar operands).
 #define OOO_INLINE __attribute__((always_inline))
 
-// Workgroup barrier without the memory-model fence __syncthreads() adds: the
-// fence would make the loader wave wait for every in-flight LDS DMA.  The
-// "memory" clobber keeps the compiler from moving LDS accesses across it.
+// Workgroup barrier without the memory-model fence __syncthreads() adds.
+// The DMA is invisible to the compiler, so waits for it are explicit
+// (wait_vmcnt) before each barrier.  The "memory" clobber keeps the compiler
+// from moving LDS accesses across it.
 __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
 // LDS DMA of 16 bytes per lane from base + voff (base wave-uniform, voff
