@@ -352,21 +352,21 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
   };
   // probabilities of one 32-key half in B-operand order; returns their sum
   auto probs_half = [&](const f32x16& acc, float m_use, bf16x8& p0, bf16x8& p1) OOO_INLINE {
-    float psum = 0.f;
+    float ps[4] = {0.f, 0.f, 0.f, 0.f};  // four independent sums: short dependency chains
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) {
       float p[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         p[e] = __builtin_amdgcn_exp2f(fmaf(acc[8 * k2 + e], a.scale_log2e, -m_use));
-        psum += p[e];
+        ps[e % 4] += p[e];
       }
       u32x4 pk;
 #pragma unroll
       for (int e = 0; e < 4; ++e) pk[e] = pack_bf16x2(p[2 * e], p[2 * e + 1]);
       (k2 == 0 ? p0 : p1) = as_bf16x8(pk);
     }
-    return psum;
+    return (ps[0] + ps[1]) + (ps[2] + ps[3]);
   };
   // Mask tile t's scores (tree tiles and ragged tails only).  Lane value j
   // of half hf is key 32(kh0+hf) + 16*(j/8) + 8u + j%8 of the tile.
@@ -391,11 +391,14 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
   auto row_max = [&](const f32x16 (&acc)[NH]) OOO_INLINE {
     float mh[NH];
 #pragma unroll
-    for (int hf = 0; hf < NH; ++hf) {
-      float m = max3f(acc[hf][0], acc[hf][1], acc[hf][2]);
-#pragma unroll
-      for (int j = 3; j < 15; j += 2) m = max3f(m, acc[hf][j], acc[hf][j + 1]);
-      mh[hf] = max3f(m, acc[hf][15], -INFINITY);
+    for (int hf = 0; hf < NH; ++hf) {  // two interleaved chains
+      float m0 = max3f(acc[hf][0], acc[hf][1], acc[hf][2]);
+      float m1 = max3f(acc[hf][8], acc[hf][9], acc[hf][10]);
+      m0 = max3f(m0, acc[hf][3], acc[hf][4]);
+      m1 = max3f(m1, acc[hf][11], acc[hf][12]);
+      m0 = max3f(m0, acc[hf][5], acc[hf][6]);
+      m1 = max3f(m1, acc[hf][13], acc[hf][14]);
+      mh[hf] = max3f(max3f(m0, acc[hf][7], m1), acc[hf][15], -INFINITY);
     }
     const float mx = NH == 2 ? max3f(mh[0], mh[NH - 1], -INFINITY) : mh[0];
     const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
