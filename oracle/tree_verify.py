@@ -234,6 +234,55 @@ def kv_compact(caches: Sequence[np.ndarray], prefix_len: int, path: np.ndarray) 
 
 
 # ----------------------------------------------------------------------------
+# O6: hint continuations and lane filling in front of the trie (Section 4.4:
+# suffix matching against the request's hint bank, n = 7 down to 1; hint
+# continuations take the candidate lanes first, the native candidates fill
+# the rest; an empty bank leaves the native candidates alone)
+
+
+def hint_continuations(bank: Sequence[int], eos: int, committed: Sequence[int], max_suffix: int,
+                       max_len: int) -> Dict:
+    """Continuations the hint bank proposes for the next position.
+
+    For n = min(max_suffix, len(committed)) down to 1, every occurrence of the
+    last n committed tokens in the bank proposes the tokens that follow it,
+    up to the next EOS (exclusive) and at most ``max_len`` of them.  The first
+    n that proposes at least one non-empty continuation is used; its
+    continuations are returned in bank order, each distinct one once.
+    """
+    bank = [int(t) for t in bank]
+    committed = [int(t) for t in committed]
+    for n in range(min(max_suffix, len(committed)), 0, -1):
+        suffix = committed[len(committed) - n:]
+        found: List[List[int]] = []
+        for j in range(0, len(bank) - n + 1):
+            if bank[j:j + n] != suffix:
+                continue
+            cont: List[int] = []
+            k = j + n
+            while k < len(bank) and bank[k] != eos and len(cont) < max_len:
+                cont.append(bank[k])
+                k += 1
+            if cont and cont not in found:
+                found.append(cont)
+        if found:
+            return {"n": n, "continuations": found}
+    return {"n": 0, "continuations": []}
+
+
+def merge_lanes(hints: Sequence[Sequence[int]], native: Sequence[Sequence[int]], n_lanes: int) -> List[List[int]]:
+    """Merge_B's lane filling: hint continuations first, then the native
+    candidates in their priority order, ``n_lanes`` candidates at most.  The
+    node budget itself is applied by pack_tree."""
+    lanes = [list(h) for h in hints][:n_lanes]
+    for c in native:
+        if len(lanes) >= n_lanes:
+            break
+        lanes.append(list(c))
+    return lanes
+
+
+# ----------------------------------------------------------------------------
 # the whole step
 
 

@@ -5,9 +5,11 @@ AssertionError on a mismatch, so the same checks run against the committed
 reference (they must pass) and against copies with a planted mistake (some
 check must fail).  What each check leans on:
 
-* hand-derived fixtures under ``golden/`` (pack, accept, compact);
+* hand-derived fixtures under ``golden/`` (pack, accept, compact, hint-bank
+  continuations and lane filling);
 * brute force: distinct-prefix enumeration for packing; causal decoding of
-  every root-to-leaf path as an ordinary sequence for attention;
+  every root-to-leaf path as an ordinary sequence for attention; a regular-
+  expression search of the hint bank for every suffix length;
 * a library routine: torch's scaled_dot_product_attention (float64, CPU)
   with an explicit boolean mask and repeat_interleave for grouped heads;
   numpy's matmul/argmax for the LM head;
@@ -435,6 +437,76 @@ def check_sequential_greedy(ov):
         np.testing.assert_allclose(vc[:, :P], Vseq[:, :P], rtol=0, atol=0)
 
 
+# ----------------------------------------------------------------------------
+# hint-bank continuations and lane filling (Section 4.4)
+
+
+def check_hint_golden(ov):
+    g = _load("hint_cases.json")
+    for c in g["hint_cases"]:
+        r = ov.hint_continuations(c["bank"], 0, c["committed"], c["max_suffix"], c["max_len"])
+        assert r["n"] == c["n"], c["name"]
+        assert [list(x) for x in r["continuations"]] == c["continuations"], c["name"]
+    for c in g["lane_cases"]:
+        assert [list(x) for x in ov.merge_lanes(c["hints"], c["native"], c["n_lanes"])] == c["lanes"]
+
+
+def _occurrences(bank, pattern):
+    """Start positions of every (overlapping) occurrence of ``pattern`` in
+    ``bank``, found by a regular-expression search over a text encoding of
+    the tokens (a different search from the reference's slicing)."""
+    import re
+    text = "".join(f"<{t}>" for t in bank)
+    pat = "".join(f"<{t}>" for t in pattern)
+    starts = [m.start() for m in re.finditer("(?=" + re.escape(pat) + ")", text)]
+    # map character offsets back to token positions
+    pos_of = {}
+    off = 0
+    for i, t in enumerate(bank):
+        pos_of[off] = i
+        off += len(f"<{t}>")
+    return [pos_of[s] for s in starts]
+
+
+def brute_hints(bank, eos, committed, max_suffix, max_len):
+    """Every n's proposals first, then the largest n that has any."""
+    per_n = {}
+    for n in range(1, min(max_suffix, len(committed)) + 1):
+        props = []
+        for j in _occurrences(bank, committed[-n:]):
+            tail = []
+            for t in bank[j + n:]:
+                if t == eos or len(tail) == max_len:
+                    break
+                tail.append(t)
+            if tail and tail not in props:
+                props.append(tail)
+        per_n[n] = props
+    best = max([n for n, props in per_n.items() if props], default=0)
+    return best, per_n.get(best, [])
+
+
+def check_hint_bruteforce(ov):
+    rs = np.random.default_rng(11)
+    for trial in range(300):
+        vocab = int(rs.integers(2, 6))  # small alphabets make long matches common
+        L = int(rs.integers(0, 60))
+        eos = 0
+        bank = [int(t) for t in rs.integers(0, vocab + 1, size=L)]  # token 0 = EOS
+        committed = [int(t) for t in rs.integers(1, vocab + 1, size=int(rs.integers(1, 10)))]
+        max_suffix = int(rs.integers(1, 8))
+        max_len = int(rs.integers(1, 6))
+        r = ov.hint_continuations(bank, eos, committed, max_suffix, max_len)
+        n, props = brute_hints(bank, eos, committed, max_suffix, max_len)
+        assert r["n"] == n, (trial, r["n"], n)
+        assert [list(x) for x in r["continuations"]] == props, trial
+        for cont in r["continuations"]:
+            assert 1 <= len(cont) <= max_len and eos not in cont
+        lanes = ov.merge_lanes(props, [[9, 9], [8]], 3)
+        assert lanes[:min(3, len(props))] == [list(x) for x in props[:3]]
+        assert len(lanes) == min(3, len(props) + 2)
+
+
 ALL_CHECKS = [
     check_pack_golden,
     check_pack_bruteforce,
@@ -448,4 +520,6 @@ ALL_CHECKS = [
     check_compact_golden,
     check_compact_gather_scatter,
     check_sequential_greedy,
+    check_hint_golden,
+    check_hint_bruteforce,
 ]

@@ -34,6 +34,17 @@ MUTATIONS = [
      "    while int(ids[cur]) in children[0] and cur == 0:\n        cur = children[0][int(ids[cur])]"),
     ("bonus_from_parent", "    bonus = int(ids[path[-1]])", "    bonus = int(ids[path[-2] if len(path) > 1 else 0])"),
     ("compact_reverse_order", "        for src, dst in pairs:", "        for src, dst in reversed(pairs):"),
+    ("hint_shortest_first", "    for n in range(min(max_suffix, len(committed)), 0, -1):",
+     "    for n in range(1, min(max_suffix, len(committed)) + 1):"),
+    ("hint_runs_through_eos", "            while k < len(bank) and bank[k] != eos and len(cont) < max_len:",
+     "            while k < len(bank) and len(cont) < max_len:"),
+    ("hint_duplicates_kept", "            if cont and cont not in found:", "            if cont:"),
+    ("hint_skips_first_token", "            k = j + n\n", "            k = j + n + 1\n"),
+    ("hint_suffix_shifted", "        suffix = committed[len(committed) - n:]",
+     "        suffix = committed[max(0, len(committed) - n - 1):len(committed) - 1]"),
+    ("hint_one_token_too_many", "and len(cont) < max_len:", "and len(cont) <= max_len:"),
+    ("lanes_native_first", "    lanes = [list(h) for h in hints][:n_lanes]\n    for c in native:",
+     "    lanes = [list(h) for h in native][:n_lanes]\n    for c in hints:"),
     ("compact_dest_by_node", "    pairs = [(prefix_len + int(path[d]), prefix_len + d) for d in range(len(path))]",
      "    pairs = [(prefix_len + int(path[d]), prefix_len + int(path[d])) for d in range(len(path))]"),
 ]
