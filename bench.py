@@ -69,6 +69,31 @@ def _source_digest(path: str) -> str:
     return hashlib.sha256(" ".join(text.split()).encode()).hexdigest()[:16]
 
 
+def time_hint_merge(cfg, cand_sets, reps: int = 200):
+    """Host time of one retrieval round's lane filling (ooo_hint_merge on a
+    request-level hint bank of eight 512-token views), per call.  Outside the
+    verify step: it runs at retrieval rounds, before ooo_pack_tree."""
+    from paper_2608_00814_amd import ooo
+    from paper_2608_00814_amd import workload as wl
+    banks = [wl.hint_bank_for(cfg, s, c) for s, c in enumerate(cand_sets)]
+    natives = []
+    for c, hb in zip(cand_sets, banks):
+        seqs = c.seqs[1:]
+        offs = np.zeros(len(seqs) + 1, np.int32)
+        for i, q in enumerate(seqs):
+            offs[i + 1] = offs[i] + len(q)
+        toks = np.array([t for q in seqs for t in q], dtype=np.int32)
+        natives.append((toks, offs, len(c.seqs)))
+        r = ooo.hint_merge(hb.bank, hb.eos, hb.committed, toks, offs, len(c.seqs), 7, cfg.max_depth)
+        lanes = [r["tokens"][r["offsets"][i]:r["offsets"][i + 1]].tolist() for i in range(r["n_out"])]
+        assert lanes == [list(q[:cfg.max_depth]) for q in c.seqs], "hint bank must reproduce the candidate lanes"
+    t0 = time.perf_counter()
+    for i in range(reps):
+        hb, (toks, offs, nl) = banks[i % len(banks)], natives[i % len(banks)]
+        ooo.hint_merge(hb.bank, hb.eos, hb.committed, toks, offs, nl, 7, cfg.max_depth)
+    return 1e6 * (time.perf_counter() - t0) / reps, int(banks[0].bank.size)
+
+
 def recorded_traffic(workload: str, entry: str):
     """HBM bytes per launch that the committed counter profile records for
     ``entry``, or None when there is none for this workload or the kernel
@@ -273,6 +298,7 @@ def main():
     tokens_per_s = float(np.sum(np.array(Ls) + 1)) / elapsed
     lm_us = 1e3 * float(np.mean(lm_ms))
     attn_us = 1e3 * float(np.mean(attn_ms))
+    hint_us, hint_tokens = time_hint_merge(cfg, cand_sets)
     attn_call_us = attn_us / cfg.n_layers
     a_bytes = attention_bytes(cfg, N)
     a_gbs = a_bytes / (attn_call_us * 1e-6) / 1e9
@@ -298,6 +324,8 @@ def main():
                    "prefix_len": P, "trie_nodes": N, "hidden": cfg.hidden, "vocab": cfg.vocab,
                    "launch": "eager" if args.no_graph else "hip-graph per phase, LM head eager"},
         "tokens_per_s": round(tokens_per_s, 1),
+        "hint_merge_us": round(hint_us, 2),
+        "hint_bank_tokens": hint_tokens,
         "mean_accepted_plus_bonus": round(float(np.mean(np.array(Ls) + 1)), 3),
         "attention_us_per_step": round(attn_us, 2),
         "attention_us_per_layer": round(attn_call_us, 3),

@@ -5,6 +5,8 @@
  * OoO-Spec paper describes it (Section 3, "Target authority" with Eq. 1 and
  * "The ToolSpec decoding loop"; Section 4.5, "Verify and commit"):
  *
+ *   ooo_hint_merge     hint-bank continuations of the committed suffix, then
+ *                      native candidates, as the lanes of one round
  *   ooo_pack_tree      merge priority-ordered draft continuations into a trie
  *   ooo_tree_attn      per layer: every trie node attends to the committed
  *                      prefix and to its own ancestors (one pass for the tree)
@@ -90,6 +92,45 @@ int ooo_pack_tree(int32_t root_token, const int32_t* cand_tokens, const int32_t*
                   int32_t n_cand, int32_t max_nodes, int32_t max_depth, int32_t* token,
                   int32_t* parent, int32_t* depth, uint64_t* anc_mask, int32_t mask_words,
                   int32_t* n_nodes, int32_t* n_truncated);
+
+/*
+ * ooo_hint_merge - candidate lanes of one retrieval round (Section 4.4,
+ * Suffix matching and Eq. 3): continuations that the request's hint bank
+ * proposes for the next position come first, the native candidates fill the
+ * remaining lanes.  The result feeds ooo_pack_tree, which applies the node
+ * budget.
+ *
+ * HOST memory only, synchronous, deterministic.
+ *   bank, bank_len   the hint bank: tokenized views separated by eos_token;
+ *                    bank_len 0 (hints not ready, or none) gives the native
+ *                    candidates alone
+ *   committed, n_committed   committed tokens, oldest first; the last one is
+ *                    the root of the next trie
+ *   max_suffix       longest suffix tried (the paper uses 7), >= 1
+ *   max_len          tokens per hint continuation, >= 1
+ *   native_tokens, native_offsets, n_native   native candidates, CSR in
+ *                    priority order (native_offsets[0] == 0, non-decreasing)
+ *   n_lanes          lanes of the round, >= 0
+ *   out_tokens       merged candidate tokens, capacity out_cap
+ *   out_offsets      [n_lanes + 1] CSR offsets of the merged candidates
+ *   n_out            merged candidates written (<= n_lanes)
+ *   n_hint           how many of them come from the bank (they come first)
+ *   suffix_len       length n of the suffix whose occurrences proposed them
+ *                    (0 when the bank proposed nothing)
+ * For n = min(max_suffix, n_committed) down to 1, every occurrence of the last
+ * n committed tokens in the bank proposes the tokens after it, up to the next
+ * eos_token (exclusive) and at most max_len of them; the first n with a
+ * non-empty proposal is used, and its proposals are taken in bank order,
+ * each distinct one once.
+ * Errors: OOO_ERR_INVALID (null pointers, negative sizes, max_suffix or
+ * max_len < 1, bad native offsets, negative tokens), OOO_ERR_CAPACITY (the
+ * merged tokens exceed out_cap; *n_out is then 0).
+ */
+int ooo_hint_merge(const int32_t* bank, int64_t bank_len, int32_t eos_token, const int32_t* committed,
+                   int32_t n_committed, int32_t max_suffix, int32_t max_len, const int32_t* native_tokens,
+                   const int32_t* native_offsets, int32_t n_native, int32_t n_lanes, int32_t* out_tokens,
+                   int64_t out_cap, int32_t* out_offsets, int32_t* n_out, int32_t* n_hint,
+                   int32_t* suffix_len);
 
 /*
  * ooo_tree_attn - one layer of tree-masked attention (Section 4.5: the target

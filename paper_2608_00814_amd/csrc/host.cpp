@@ -105,3 +105,86 @@ extern "C" int ooo_pack_tree(int32_t root_token, const int32_t* cand_tokens,
     return ooo::fail(OOO_ERR_INVALID, "ooo_pack_tree: internal error");
   }
 }
+
+// Lanes of one retrieval round (Section 4.4, Suffix matching; Eq. 3).  One
+// pass over the bank computes, for every position i, the longest k <=
+// max_suffix with bank[i-k, i) equal to the last k committed tokens; the
+// suffix length used is the largest k at a position that starts a non-empty
+// continuation (not EOS, not the bank end), and every such position with at
+// least that match proposes its continuation, in bank order.
+extern "C" int ooo_hint_merge(const int32_t* bank, int64_t bank_len, int32_t eos_token, const int32_t* committed,
+                              int32_t n_committed, int32_t max_suffix, int32_t max_len,
+                              const int32_t* native_tokens, const int32_t* native_offsets, int32_t n_native,
+                              int32_t n_lanes, int32_t* out_tokens, int64_t out_cap, int32_t* out_offsets,
+                              int32_t* n_out, int32_t* n_hint, int32_t* suffix_len) {
+  try {
+    OOO_REQUIRE(n_out && n_hint && suffix_len && out_offsets, OOO_ERR_INVALID, "ooo_hint_merge: null output");
+    *n_out = 0;
+    *n_hint = 0;
+    *suffix_len = 0;
+    OOO_REQUIRE(bank_len >= 0 && n_committed >= 0 && n_native >= 0 && n_lanes >= 0 && out_cap >= 0,
+                OOO_ERR_INVALID, "ooo_hint_merge: negative size");
+    OOO_REQUIRE(bank_len == 0 || bank, OOO_ERR_INVALID, "ooo_hint_merge: bank is null");
+    OOO_REQUIRE(n_committed == 0 || committed, OOO_ERR_INVALID, "ooo_hint_merge: committed is null");
+    OOO_REQUIRE(max_suffix >= 1 && max_len >= 1, OOO_ERR_INVALID,
+                "ooo_hint_merge: max_suffix (%d) and max_len (%d) must be >= 1", max_suffix, max_len);
+    OOO_REQUIRE(native_offsets, OOO_ERR_INVALID, "ooo_hint_merge: native_offsets is null");
+    OOO_REQUIRE(native_offsets[0] == 0, OOO_ERR_INVALID, "ooo_hint_merge: native_offsets[0] must be 0");
+    for (int32_t c = 0; c < n_native; ++c)
+      OOO_REQUIRE(native_offsets[c + 1] >= native_offsets[c], OOO_ERR_INVALID,
+                  "ooo_hint_merge: native_offsets must be non-decreasing (at %d)", c);
+    OOO_REQUIRE(native_offsets[n_native] == 0 || native_tokens, OOO_ERR_INVALID,
+                "ooo_hint_merge: native_tokens is null");
+    for (int32_t t = 0; t < native_offsets[n_native]; ++t)
+      OOO_REQUIRE(native_tokens[t] >= 0, OOO_ERR_INVALID, "ooo_hint_merge: negative native token at %d", t);
+    OOO_REQUIRE(n_lanes == 0 || out_cap == 0 || out_tokens, OOO_ERR_INVALID, "ooo_hint_merge: out_tokens is null");
+
+    const int32_t K = max_suffix < n_committed ? max_suffix : n_committed;
+    const int32_t* tail = committed + n_committed;  // tail[-k] is the k-th last committed token
+    auto match_before = [&](int64_t i) {           // longest k with bank[i-k, i) == last k committed
+      int32_t k = 0;
+      while (k < K && i - k - 1 >= 0 && bank[i - k - 1] == tail[-k - 1]) ++k;
+      return k;
+    };
+    auto starts_proposal = [&](int64_t i) { return i < bank_len && bank[i] != eos_token; };
+    int32_t best = 0;
+    if (K > 0)
+      for (int64_t i = 1; i < bank_len && best < K; ++i)
+        if (starts_proposal(i)) {
+          const int32_t k = match_before(i);
+          if (k > best) best = k;
+        }
+
+    std::vector<std::vector<int32_t>> lanes;
+    if (best > 0)
+      for (int64_t i = best; i < bank_len && (int32_t)lanes.size() < n_lanes; ++i) {
+        if (!starts_proposal(i) || match_before(i) < best) continue;
+        std::vector<int32_t> cont;
+        for (int64_t j = i; j < bank_len && bank[j] != eos_token && (int32_t)cont.size() < max_len; ++j)
+          cont.push_back(bank[j]);
+        bool seen = false;
+        for (const auto& l : lanes) seen = seen || l == cont;
+        if (!seen) lanes.push_back(std::move(cont));
+      }
+    const int32_t hints = (int32_t)lanes.size();
+    for (int32_t c = 0; c < n_native && (int32_t)lanes.size() < n_lanes; ++c)
+      lanes.emplace_back(native_tokens + native_offsets[c], native_tokens + native_offsets[c + 1]);
+
+    int64_t total = 0;
+    for (const auto& l : lanes) total += (int64_t)l.size();
+    OOO_REQUIRE(total <= out_cap, OOO_ERR_CAPACITY, "ooo_hint_merge: %lld merged tokens exceed out_cap %lld",
+                (long long)total, (long long)out_cap);
+    int64_t pos = 0;
+    out_offsets[0] = 0;
+    for (size_t c = 0; c < lanes.size(); ++c) {
+      for (int32_t t : lanes[c]) out_tokens[pos++] = t;
+      out_offsets[c + 1] = (int32_t)pos;
+    }
+    *n_out = (int32_t)lanes.size();
+    *n_hint = hints;
+    *suffix_len = best;
+    return ooo::ok();
+  } catch (...) {
+    return ooo::fail(OOO_ERR_INVALID, "ooo_hint_merge: internal error");
+  }
+}

@@ -34,6 +34,8 @@ SIGNATURES = {
     "ooo_version": (ctypes.c_int, []),
     "ooo_pack_tree": (ctypes.c_int, [_i32, _c_i32p, _c_i32p, _i32, _i32, _i32, _c_i32p, _c_i32p, _c_i32p,
                                      _c_u64p, _i32, _c_i32p, _c_i32p]),
+    "ooo_hint_merge": (ctypes.c_int, [_c_i32p, _i64, _i32, _c_i32p, _i32, _i32, _i32, _c_i32p, _c_i32p, _i32,
+                                      _i32, _c_i32p, _i64, _c_i32p, _c_i32p, _c_i32p, _c_i32p]),
     "ooo_tree_attn_workspace": (_sz, [_i32, _i32, _i32, _i32, _i32, ctypes.c_int]),
     "ooo_tree_attn": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _i32, _vp, _i32, _i32, _i32, _i32,
                                      ctypes.c_float, ctypes.c_int, _vp, _vp, _sz, _vp]),
@@ -141,6 +143,29 @@ def pack_tree(root_token: int, cand_tokens: np.ndarray, cand_offsets: np.ndarray
     return {"token": token[:k].copy(), "parent": parent[:k].copy(), "depth": depth[:k].copy(),
             "anc_mask": mask.reshape(cap, W)[:k].copy(), "n_nodes": k, "n_truncated": trunc.value,
             "mask_words": W}
+
+
+def hint_merge(bank: np.ndarray, eos_token: int, committed: np.ndarray, native_tokens: np.ndarray,
+               native_offsets: np.ndarray, n_lanes: int, max_suffix: int = 7, max_len: int = 64) -> dict:
+    """ooo_hint_merge on NumPy arrays: the merged lanes as CSR (tokens,
+    offsets), plus how many came from the bank and the suffix length used."""
+    b = np.ascontiguousarray(bank, dtype=np.int32)
+    cm = np.ascontiguousarray(committed, dtype=np.int32)
+    nt = np.ascontiguousarray(native_tokens, dtype=np.int32)
+    no = np.ascontiguousarray(native_offsets, dtype=np.int32)
+    cap = int(nt.size) + int(n_lanes) * int(max_len)
+    out = np.zeros(max(cap, 1), np.int32)
+    offs = np.zeros(int(n_lanes) + 1, np.int32)
+    n_out, n_hint, slen = ctypes.c_int32(0), ctypes.c_int32(0), ctypes.c_int32(0)
+    p = lambda a: a.ctypes.data_as(_c_i32p) if a.size else None
+    st = lib().ooo_hint_merge(p(b), int(b.size), int(eos_token), p(cm), int(cm.size), int(max_suffix),
+                              int(max_len), p(nt), no.ctypes.data_as(_c_i32p), len(no) - 1, int(n_lanes),
+                              out.ctypes.data_as(_c_i32p), cap, offs.ctypes.data_as(_c_i32p), ctypes.byref(n_out),
+                              ctypes.byref(n_hint), ctypes.byref(slen))
+    _check(st)
+    k = n_out.value
+    return {"tokens": out[:offs[k]].copy(), "offsets": offs[:k + 1].copy(), "n_out": k, "n_hint": n_hint.value,
+            "suffix_len": slen.value}
 
 
 # ----------------------------------------------------------------------------

@@ -48,6 +48,7 @@ S_LMW = 6
 S_HIDDEN = 7
 S_TAU = 8
 S_PLANT = 9
+S_BANK = 10
 
 # boost applied to the designated token's weight direction in a hidden row
 HIDDEN_BOOST = 12.0
@@ -281,6 +282,41 @@ def _fresh_seq(g: np.random.Generator, vocab: int, n: int, first_avoid: Sequence
     if n <= 0:
         return []
     return [_fresh(g, vocab, first_avoid)] + [int(t) for t in g.integers(0, vocab, size=n - 1)]
+
+
+@dataclasses.dataclass
+class HintBank:
+    """A request-level hint bank (Section 4.4, Tokenizer and hint bank):
+    tokenized views joined by ``eos``, plus the committed tokens (oldest
+    first, ending with the root) whose suffix the bank continues."""
+
+    bank: np.ndarray
+    eos: int
+    committed: np.ndarray
+    hint_lanes: int  # leading candidates that the bank holds
+
+
+def hint_bank_for(cfg: VerifyConfig, seed: int, cand: Candidates, step: int = 0, n_views: int = 8,
+                  view_len: int = 512, history: int = 16) -> HintBank:
+    """Random views of ``view_len`` tokens separated by EOS (token vocab-1);
+    one view holds the last seven committed tokens followed by the step's
+    first candidate (the hint lane) and then EOS, so the bank proposes that
+    candidate for this position.  The other candidates are the native lanes.
+    Only the first candidate is planted: recipes whose first candidate is not
+    a hint still get a bank, and the finder then proposes it as well."""
+    g = rng(cfg, seed, step, S_BANK)
+    eos = cfg.vocab - 1
+    committed = [int(t) for t in g.integers(0, eos, size=history - 1)] + [int(cand.root_token)]
+    views = [[int(t) for t in g.integers(0, eos, size=view_len)] for _ in range(n_views)]
+    hint = list(cand.seqs[0]) if cand.seqs else []
+    at = int(g.integers(0, n_views))
+    plant = committed[-7:] + hint
+    pos = int(g.integers(0, max(1, view_len - len(plant))))
+    views[at] = views[at][:pos] + plant + [eos]
+    bank = []
+    for v in views:
+        bank += v + [eos]
+    return HintBank(np.array(bank, dtype=np.int32), eos, np.array(committed, dtype=np.int32), 1 if hint else 0)
 
 
 def candidates_for(cfg: VerifyConfig, seed: int, step: int = 0, root_token: Optional[int] = None) -> Candidates:
