@@ -262,7 +262,7 @@ def main():
 
         def one_step(i, timed):
             v = i % n_variants
-            runner.pack(cand_sets[v].root_token, *csr[v])
+            runner.pack(cand_sets[v].root_token, *csr[v], keep=False)
             runner.upload_tree()
             ev[0].record(stream)
             if graphs:

@@ -5,7 +5,11 @@
 // W from HBM once; it is bound by HBM bandwidth, so the design is about
 // keeping enough whole cache lines in flight:
 //  * A persistent grid (one block per CU) walks 128-row vocabulary tiles
-//    round-robin; the K dimension is cut into 64-element chunks.
+//    round-robin; the K dimension is cut into 64-element chunks.  The last,
+//    partial round of tiles is dealt out in 32-row groups (one per compute
+//    wave), so that no block streams more than one group beyond the average
+//    (1187 tiles on 256 blocks: 4 tiles + 2 or 3 groups each, instead of 4
+//    or 5 tiles).
 //  * Two loader waves copy each chunk of W (128 rows x 128 B) and of X
 //    (all nodes x 128 B) from global memory straight into a 3-5 stage LDS
 //    ring with global_load_lds: every DMA instruction moves 8 whole rows.
@@ -45,16 +49,17 @@ __device__ __forceinline__ void wait_vmcnt() {
 constexpr int kLmRows = 128;  // vocabulary rows per tile (4 waves x 32)
 
 // Ring of NS stages; NS - 2 chunks are in flight while one is consumed.
-// Wider node tiles need more X bytes per stage, so fewer stages fit.
+// Wider node tiles need more X bytes per stage, so fewer stages fit.  Two
+// loader waves split each W chunk (two 32-row slots each), a third loads X.
 template <int NB>
 struct LmRing {
   static constexpr int XR = 32 * NB;            // node rows staged (padded)
   static constexpr int WS = kLmRows * 128;      // bytes of a W chunk
   static constexpr int XS = XR * 128;           // bytes of an X chunk
-  static constexpr int NS = NB <= 2 ? 5 : NB == 4 ? 4 : 3;
+  static constexpr int NS = NB == 1 ? 7 : NB == 2 ? 6 : NB == 4 ? 4 : 3;
   static constexpr int XREG = NS * WS;          // start of the X stages
   static constexpr int BYTES = NS * (WS + XS);
-  static constexpr int WDMA = WS / 1024;        // DMA instructions per W chunk
+  static constexpr int WDMA = WS / 1024 / 2;    // DMA instructions per W chunk and W loader
   static constexpr int XDMA = XS / 1024;
   static_assert((NS - 2) * WDMA <= 63 && (NS - 2) * XDMA <= 63, "vmcnt range");
   static_assert(BYTES + 4 * 32 * NB * 8 <= 160 * 1024, "LDS capacity");
@@ -63,14 +68,17 @@ struct LmRing {
 // wait until at most `ahead` chunks of `per` DMA instructions are pending
 template <int PER, int MAXA>
 __device__ __forceinline__ void wait_chunks(int ahead) {
-  if (MAXA >= 3 && ahead >= 3) wait_vmcnt<(MAXA >= 3 ? 3 * PER : 0)>();
+  static_assert(MAXA <= 5, "ring depth");
+  if (MAXA >= 5 && ahead >= 5) wait_vmcnt<(MAXA >= 5 ? 5 * PER : 0)>();
+  else if (MAXA >= 4 && ahead == 4) wait_vmcnt<(MAXA >= 4 ? 4 * PER : 0)>();
+  else if (MAXA >= 3 && ahead == 3) wait_vmcnt<(MAXA >= 3 ? 3 * PER : 0)>();
   else if (MAXA >= 2 && ahead == 2) wait_vmcnt<(MAXA >= 2 ? 2 * PER : 0)>();
   else if (ahead == 1) wait_vmcnt<PER>();
   else wait_vmcnt<0>();
 }
 
 template <int NB, bool PACKED>
-__global__ __launch_bounds__(384) void lmhead_bf16_kernel(const uint16_t* __restrict__ X,
+__global__ __launch_bounds__(448) void lmhead_bf16_kernel(const uint16_t* __restrict__ X,
                                                           const uint16_t* __restrict__ Wt, int N, int H, int V,
                                                           Cand* __restrict__ partial, float* __restrict__ logits) {
   using R = LmRing<NB>;
@@ -78,32 +86,76 @@ __global__ __launch_bounds__(384) void lmhead_bf16_kernel(const uint16_t* __rest
   __shared__ Cand red[4][32 * NB];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int chunks = H / 64;
+  const int b = (int)blockIdx.x, grid = (int)gridDim.x;
   const int ntiles_all = (V + kLmRows - 1) / kLmRows;
-  const int my_tiles = ntiles_all > (int)blockIdx.x ? (ntiles_all - 1 - (int)blockIdx.x) / (int)gridDim.x + 1 : 0;
+  const int full_rounds = ntiles_all / grid;                  // rounds of whole tiles for every block
+  const int rem_groups = (ntiles_all - full_rounds * grid) * 4;  // 32-row groups of the last round
+  const int my_tiles = full_rounds + (rem_groups > b ? 1 : 0);
   const int total = my_tiles * chunks;  // chunks this block streams
+  // 32-row group of slot s (compute wave s) in the block's tile t, or -1
+  auto group_of = [&](int t, int s) {
+    if (t < full_rounds) return 4 * (b + t * grid) + s;
+    const int rg = b + s * grid;
+    return rg < rem_groups ? 4 * full_rounds * grid + rg : -1;
+  };
 
   if (wave >= 4) {
-    // ---------------------------------------------------- loaders: W (4), X (5)
-    const bool is_x = wave == 5;
+    // -------------------------------------- loaders: W slots 0-1 (4), 2-3 (5), X (6)
+    const bool is_x = wave == 6;
+    const int s_lo = 2 * (wave - 4);  // first W slot of this loader
+    // Per-slot source of the tile whose chunks are being issued, set once
+    // per tile: the group's first chunk and the element step per chunk.  An
+    // empty slot (last round only) copies a line of X instead (step 0),
+    // which sits in L2, so that every chunk is the same number of DMA
+    // instructions.
+    int issue_tile = -1;
+    const uint16_t* sbase[4];
+    int sstep[4];
+    auto set_tile = [&](int t) {
+#pragma unroll
+      for (int s4 = 0; s4 < 4; ++s4) {
+        const int gi = group_of(t, s4);
+        if (gi < 0) {
+          sbase[s4] = X + (size_t)(b % N) * H + min(lane * 8, H - 8);
+          sstep[s4] = 0;
+        } else if (PACKED) {
+          // the group's chunk is a contiguous 4 KiB run of the tile's 16 KiB
+          // block, already swizzled
+          sbase[s4] = Wt + ((size_t)(gi / 4) * chunks * kLmRows + 32 * (gi % 4)) * 64 + lane * 8;
+          sstep[s4] = kLmRows * 64;
+        } else {
+          sbase[s4] = Wt + (size_t)32 * gi * H;  // group row 0; rows and pieces per lane below
+          sstep[s4] = 64;
+        }
+      }
+      issue_tile = t;
+    };
     auto issue = [&](int q, int stage) {
-      const int tile = (int)blockIdx.x + (q / chunks) * (int)gridDim.x;
+      const int t = q / chunks;
       const int kc = q % chunks;
       if (!is_x) {
         uint8_t* dst = lds + stage * R::WS;
-        if (PACKED) {
-          // the chunk is one contiguous 16 KiB block, already swizzled
-          const uint16_t* src = Wt + ((size_t)tile * chunks + kc) * (kLmRows * 64) + lane * 8;
+        if (t != issue_tile) set_tile(t);
+        // DMA instruction j fills rows 8j .. 8j+7 of the stage: slot j / 4
 #pragma unroll
-          for (int j = 0; j < R::WDMA; ++j)
-            __builtin_amdgcn_global_load_lds(OOO_GLB(src + j * 512), OOO_LDS(dst + j * 1024), 16, 0, 0);
-        } else {
+        for (int s4 = 0; s4 < 4; ++s4) {
+          if (s4 / 2 != s_lo / 2) continue;
+          const uint16_t* src = sbase[s4] + kc * sstep[s4];
+          if (PACKED || sstep[s4] == 0) {
 #pragma unroll
-          for (int j = 0; j < R::WDMA; ++j) {
-            const int r = 8 * j + lane / 8;  // tile row; lane = (row, physical piece)
-            const int pc = (lane % 8) ^ (r % 8);
-            const int row = min(tile * kLmRows + r, V - 1);
-            __builtin_amdgcn_global_load_lds(OOO_GLB(Wt + (size_t)row * H + kc * 64 + pc * 8),
-                                             OOO_LDS(dst + j * 1024), 16, 0, 0);
+            for (int jj = 0; jj < 4; ++jj)
+              __builtin_amdgcn_global_load_lds(OOO_GLB(src + (sstep[s4] ? jj * 512 : 0)),
+                                               OOO_LDS(dst + (4 * s4 + jj) * 1024), 16, 0, 0);
+          } else {
+            const int gi = group_of(t, s4);
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+              const int r = 8 * jj + lane / 8;  // group row; lane = (row, physical piece)
+              const int pc = (lane % 8) ^ (r % 8);
+              const int row = min(32 * gi + r, V - 1);
+              __builtin_amdgcn_global_load_lds(OOO_GLB(Wt + (size_t)row * H + kc * 64 + pc * 8),
+                                               OOO_LDS(dst + (4 * s4 + jj) * 1024), 16, 0, 0);
+            }
           }
         }
       } else {
@@ -145,14 +197,17 @@ __global__ __launch_bounds__(384) void lmhead_bf16_kernel(const uint16_t* __rest
     besti[nb] = 0x7FFFFFFF;
   }
   f32x16 acc[NB];
+  int gi = -1;  // this wave's 32-row group in the current tile
   for (int q = 0; q < total; ++q) {
     const int kc = q % chunks;
     if (kc == 0) {
+      gi = group_of(q / chunks, wave);
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x16{};
     }
     const int stage = q % R::NS;
     wg_barrier();
+    if (gi < 0) continue;  // empty slot of the last round (barriers only)
     const uint8_t* Ws = lds + stage * R::WS + wrow;
     const uint8_t* Xs = lds + R::XREG + stage * R::XS;
     bf16x8 af[4], bf[NB][4];
@@ -169,8 +224,7 @@ __global__ __launch_bounds__(384) void lmhead_bf16_kernel(const uint16_t* __rest
 
     if (kc == chunks - 1) {
       // tile done: acc[nb][j] = logit of vocabulary row v0 + 8(j/4) + 4u + j%4, node 32nb + c
-      const int tile = (int)blockIdx.x + (q / chunks) * (int)gridDim.x;
-      const int v0 = tile * kLmRows + wave * 32;
+      const int v0 = 32 * gi;
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
         float bv = -INFINITY;
@@ -371,9 +425,9 @@ extern "C" int ooo_lmhead_argmax(const void* hidden, const void* weight, int32_t
 #define OOO_LM_LAUNCH(NBV)                                                                                   \
   do {                                                                                                      \
     if (pk)                                                                                                 \
-      lmhead_bf16_kernel<NBV, true><<<p.blocks, 384, 0, st>>>(X, W, n_nodes, hidden_dim, vocab, part, logits); \
+      lmhead_bf16_kernel<NBV, true><<<p.blocks, 448, 0, st>>>(X, W, n_nodes, hidden_dim, vocab, part, logits); \
     else                                                                                                    \
-      lmhead_bf16_kernel<NBV, false><<<p.blocks, 384, 0, st>>>(X, W, n_nodes, hidden_dim, vocab, part, logits); \
+      lmhead_bf16_kernel<NBV, false><<<p.blocks, 448, 0, st>>>(X, W, n_nodes, hidden_dim, vocab, part, logits); \
   } while (0)
     if (p.nb == 1) OOO_LM_LAUNCH(1);
     else if (p.nb == 2) OOO_LM_LAUNCH(2);

@@ -145,6 +145,30 @@ def pack_tree(root_token: int, cand_tokens: np.ndarray, cand_offsets: np.ndarray
             "mask_words": W}
 
 
+def pack_tree_into(root_token: int, cand_tokens: np.ndarray, cand_offsets: np.ndarray, max_nodes: int,
+                   max_depth: int, token: np.ndarray, parent: np.ndarray, depth: np.ndarray,
+                   anc_mask: np.ndarray) -> tuple:
+    """ooo_pack_tree writing straight into caller arrays (for example views
+    of a pinned staging buffer): token/parent/depth int32 [>= max_nodes],
+    anc_mask uint64 [>= max_nodes][W], all C-contiguous.  Returns
+    (n_nodes, n_truncated)."""
+    for a, nm, dt in ((token, "token", np.int32), (parent, "parent", np.int32), (depth, "depth", np.int32),
+                      (anc_mask, "anc_mask", np.uint64)):
+        if a.dtype != dt or not a.flags.c_contiguous or a.shape[0] < max_nodes:
+            raise ValueError(f"{nm} must be a C-contiguous {np.dtype(dt).name} array of >= {max_nodes} rows")
+    W = 1 if anc_mask.ndim == 1 else int(anc_mask.shape[1])
+    toks = np.ascontiguousarray(cand_tokens, dtype=np.int32)
+    offs = np.ascontiguousarray(cand_offsets, dtype=np.int32)
+    n = ctypes.c_int32(0)
+    trunc = ctypes.c_int32(0)
+    _check(lib().ooo_pack_tree(int(root_token), toks.ctypes.data_as(_c_i32p) if toks.size else None,
+                               offs.ctypes.data_as(_c_i32p), len(offs) - 1, int(max_nodes), int(max_depth),
+                               token.ctypes.data_as(_c_i32p), parent.ctypes.data_as(_c_i32p),
+                               depth.ctypes.data_as(_c_i32p), anc_mask.ctypes.data_as(_c_u64p), W,
+                               ctypes.byref(n), ctypes.byref(trunc)))
+    return n.value, trunc.value
+
+
 def hint_merge(bank: np.ndarray, eos_token: int, committed: np.ndarray, native_tokens: np.ndarray,
                native_offsets: np.ndarray, n_lanes: int, max_suffix: int = 7, max_len: int = 64) -> dict:
     """ooo_hint_merge on NumPy arrays: the merged lanes as CSR (tokens,

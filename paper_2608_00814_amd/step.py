@@ -58,6 +58,11 @@ class VerifyRunner:
         self.token = self.d_tree[m:m + n]
         self.parent = self.d_tree[m + n:m + 2 * n]
         self.depth = self.d_tree[m + 2 * n:m + 3 * n]
+        h = self.h_tree.numpy()
+        self._h_mask = h[0:m].view(np.uint64).reshape(n, self.W)
+        self._h_token = h[m:m + n]
+        self._h_parent = h[m + n:m + 2 * n]
+        self._h_depth = h[m + 2 * n:m + 3 * n]
         self.out = torch.empty(n_layers, max_nodes, n_q_heads, head_dim, dtype=dtype, device=dev)
         self.ids = torch.empty(max_nodes, dtype=torch.int32, device=dev)
         self.max_logit = torch.empty(max_nodes, dtype=torch.float32, device=dev)
@@ -73,22 +78,25 @@ class VerifyRunner:
         self.lm_ws = torch.empty(max(lws, 256) // 4 + 1, dtype=torch.float32, device=dev)
         self.scale = 1.0 / math.sqrt(head_dim)
         self.n_nodes = 0
+        self.n_truncated = 0
         self.packed = None
 
     # -- host ---------------------------------------------------------------
-    def pack(self, root_token: int, cand_tokens: np.ndarray, cand_offsets: np.ndarray) -> dict:
-        p = ooo.pack_tree(root_token, cand_tokens, cand_offsets, self.max_nodes, self.max_depth, self.W)
-        n = self.max_nodes
-        m = 2 * n * self.W
-        h = self.h_tree.numpy()
-        k = p["n_nodes"]
-        h[0:m].view(np.uint64).reshape(n, self.W)[:k] = p["anc_mask"]
-        h[m:m + k] = p["token"]
-        h[m + n:m + n + k] = p["parent"]
-        h[m + 2 * n:m + 2 * n + k] = p["depth"]
+    def pack(self, root_token: int, cand_tokens: np.ndarray, cand_offsets: np.ndarray,
+             keep: bool = True) -> Optional[dict]:
+        """Pack the candidates straight into the pinned staging buffer.  With
+        keep, also return copies of the trie arrays (the buffer is rewritten
+        by the next pack); without, return None (the per-step path)."""
+        k, trunc = ooo.pack_tree_into(root_token, cand_tokens, cand_offsets, self.max_nodes, self.max_depth,
+                                      self._h_token, self._h_parent, self._h_depth, self._h_mask)
         self.n_nodes = k
-        self.packed = p
-        return p
+        self.n_truncated = trunc
+        self.packed = None
+        if keep:
+            self.packed = {"token": self._h_token[:k].copy(), "parent": self._h_parent[:k].copy(),
+                           "depth": self._h_depth[:k].copy(), "anc_mask": self._h_mask[:k].copy(),
+                           "n_nodes": k, "n_truncated": trunc, "mask_words": self.W}
+        return self.packed
 
     def ensure_workspace(self, prefix_len: int, n_nodes: Optional[int] = None) -> None:
         """Grow the attention workspace (outside any timed or captured region)."""
@@ -124,8 +132,7 @@ class VerifyRunner:
     def result(self) -> StepResult:
         r = self.h_res.numpy()
         L = int(r[0])
-        return StepResult(self.n_nodes, int(self.packed["n_truncated"]) if self.packed else 0, L, int(r[1]),
-                          r[2:2 + L + 1].copy())
+        return StepResult(self.n_nodes, self.n_truncated, L, int(r[1]), r[2:2 + L + 1].copy())
 
     def set_weight(self, weight, packed: Optional[bool] = None) -> None:
         """Binds the LM-head weight [V][H].  bf16 weights are re-laid out once

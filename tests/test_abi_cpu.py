@@ -83,6 +83,31 @@ def test_pack_matches_reference_on_workloads(name):
             _assert_same(*_pack_both(c.root_token, c.seqs, c.max_nodes, c.max_depth, cfg.mask_words))
 
 
+def test_pack_into_caller_buffers_matches_reference():
+    """The in-place packer (writing into one reused staging buffer, as the
+    per-step runner does) gives the same trie as the oracle for a sequence of
+    different candidate sets, whatever the buffer held before."""
+    max_nodes, W = 64, 1
+    buf = np.full(3 * max_nodes + 2 * max_nodes * W, -7, np.int32)
+    m = 2 * max_nodes * W
+    mask = buf[0:m].view(np.uint64).reshape(max_nodes, W)
+    tok, par, dep = buf[m:m + max_nodes], buf[m + max_nodes:m + 2 * max_nodes], buf[m + 2 * max_nodes:]
+    for root, cands, _, md in oc.random_candidate_sets(5, count=60):
+        offs = np.zeros(len(cands) + 1, np.int32)
+        for i, c in enumerate(cands):
+            offs[i + 1] = offs[i] + len(c)
+        toks = np.array([t for c in cands for t in c], dtype=np.int32)
+        n, trunc = ooo.pack_tree_into(root, toks, offs, max_nodes, md, tok, par, dep, mask)
+        ref = ov.pack_tree(root, cands, max_nodes, md)
+        assert n == ref["n_nodes"] and trunc == ref["n_truncated"]
+        assert np.array_equal(tok[:n], ref["token"]) and np.array_equal(par[:n], ref["parent"])
+        assert np.array_equal(dep[:n], ref["depth"])
+        assert np.array_equal(mask[:n], ov.ancestor_masks(ref["parent"], W))
+    with pytest.raises(ValueError):
+        ooo.pack_tree_into(1, np.array([2], np.int32), np.array([0, 1], np.int32), max_nodes, 4,
+                           tok[:10], par, dep, mask)
+
+
 def test_pack_degenerate_inputs():
     r, ref = _pack_both(3, [], 1, 0)
     _assert_same(r, ref)
