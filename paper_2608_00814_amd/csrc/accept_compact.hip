@@ -24,6 +24,11 @@ namespace {
 
 constexpr int kMaxMaskWords = 16;
 
+// All inputs are read once, with every load issued up front (one round trip
+// to memory); the parent's greedy token and the bonus are then looked up in
+// LDS.  Depths of accepted nodes are below n_nodes <= 1024, so path entries
+// from 1024 on are always -1.
+constexpr int kMaxNodes = 64 * kMaxMaskWords;
 __global__ __launch_bounds__(1024) void accept_kernel(const int32_t* __restrict__ token,
                                                       const int32_t* __restrict__ parent,
                                                       const int32_t* __restrict__ depth,
@@ -32,37 +37,46 @@ __global__ __launch_bounds__(1024) void accept_kernel(const int32_t* __restrict_
                                                       int32_t* __restrict__ path, int32_t* __restrict__ accept_len,
                                                       int32_t* __restrict__ bonus) {
   __shared__ uint64_t match[kMaxMaskWords];
+  __shared__ int32_t ids_s[kMaxNodes];
+  __shared__ int32_t path_s[kMaxNodes];
   __shared__ int best_depth;
   const int tid = threadIdx.x;
+  const int i = tid;  // one thread per node (blockDim = 64 * W >= N)
+  int tk = 0, pa = 0, dp = 0;
+  uint64_t am[kMaxMaskWords];
+  if (i < N) {
+    tk = token[i];
+    pa = parent[i];
+    dp = depth[i];
+    ids_s[i] = ids[i];
+#pragma unroll
+    for (int w = 0; w < kMaxMaskWords; ++w)
+      if (w < W) am[w] = anc[(size_t)i * W + w];
+  }
+  for (int k = tid; k < kMaxNodes; k += blockDim.x) path_s[k] = -1;
   if (tid == 0) best_depth = 0;
-  for (int i = tid; i < path_cap; i += blockDim.x) path[i] = -1;
-  for (int w = tid; w < W; w += blockDim.x) match[w] = 0;
   __syncthreads();
   // match bits, one ballot per 64 nodes
-  for (int base = 0; base < 64 * W; base += blockDim.x) {
-    const int i = base + tid;
-    bool m = false;
-    if (i < N) m = (i == 0) || (token[i] == ids[parent[i]]);
-    const uint64_t bits = __ballot(m);
-    if ((tid & 63) == 0 && i < 64 * W) match[i >> 6] = bits;
-  }
+  const bool m = i < N && (i == 0 || (pa >= 0 && pa < N && tk == ids_s[pa]));
+  const uint64_t bits = __ballot(m);
+  if ((tid & 63) == 0 && tid < 64 * W) match[tid >> 6] = bits;
   __syncthreads();
-  for (int i = tid; i < N; i += blockDim.x) {
+  if (i < N) {
     bool ok = true;
-    for (int w = 0; w < W; ++w) ok = ok && ((anc[(size_t)i * W + w] & ~match[w]) == 0);
-    if (ok) {
-      const int d = depth[i];
-      if (d < path_cap) {
-        path[d] = i;
-        atomicMax(&best_depth, d);
-      }
+#pragma unroll
+    for (int w = 0; w < kMaxMaskWords; ++w)
+      if (w < W) ok = ok && ((am[w] & ~match[w]) == 0);
+    if (ok && dp < path_cap && dp < kMaxNodes) {
+      path_s[dp] = i;
+      atomicMax(&best_depth, dp);
     }
   }
   __syncthreads();
+  for (int k = tid; k < path_cap; k += blockDim.x) path[k] = k < kMaxNodes ? path_s[k] : -1;
   if (tid == 0) {
     const int L = best_depth;
     *accept_len = L;
-    *bonus = ids[path[L]];
+    *bonus = ids_s[path_s[L]];
   }
 }
 
@@ -72,11 +86,20 @@ __global__ __launch_bounds__(256) void kv_compact_kernel(uint8_t* __restrict__ k
                                                          const int32_t* __restrict__ accept_len, int path_cap) {
   const int slice = blockIdx.x;  // (layer * Hkv + head) * 2 + (K or V)
   uint8_t* base = ((slice & 1) ? v : k) + (size_t)(slice >> 1) * cap * row_bytes;
-  int L = *accept_len;
-  if (L > path_cap - 1) L = path_cap - 1;
   const int chunks = row_bytes / 16;  // 16-byte pieces per row
   constexpr int R = 4;                // pieces per thread per pass
   const int rows_per_pass = (256 * R) / chunks;
+  // The first pass's path entries are read together with the accepted
+  // length (one round trip instead of two); entries past it go unused.
+  int first_src[R];
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    const int item = threadIdx.x + 256 * i;
+    const int d = 1 + item / chunks;
+    first_src[i] = (item < rows_per_pass * chunks && d < path_cap && d < N) ? path[d] : -1;
+  }
+  int L = *accept_len;
+  if (L > path_cap - 1) L = path_cap - 1;
   for (int d0 = 1; d0 <= L; d0 += rows_per_pass) {
     u32x4 buf[R];
     int dst[R];
@@ -86,7 +109,7 @@ __global__ __launch_bounds__(256) void kv_compact_kernel(uint8_t* __restrict__ k
       const int d = d0 + item / chunks, ch = item % chunks;
       dst[i] = -1;
       if (item < rows_per_pass * chunks && d <= L && d < N) {
-        const int src = path[d];
+        const int src = d0 == 1 ? first_src[i] : path[d];
         if (src >= 0 && src < N) {
           buf[i] = ld16(base + (size_t)(P + src) * row_bytes + 16 * ch);
           dst[i] = d;

@@ -1,7 +1,6 @@
 // Host-only part of libooo: error reporting, version and trie packing.
 #include <cstdio>
 #include <cstring>
-#include <unordered_map>
 #include <vector>
 
 #include "ooo_internal.h"
@@ -31,9 +30,12 @@ extern "C" int ooo_version(void) { return OOO_ABI_VERSION; }
 
 // Candidate trie (Section 3, ToolSpec loop; Section 4.4, fixed candidate
 // budget with hint lanes first; Section 4.5, one candidate tree).  Children
-// are found through a hash map keyed by (parent, token); the ancestor bitmask
-// of a node is its parent's mask plus its own bit, which is valid because a
-// parent is always created before its children.
+// are found by walking the parent's child list (first child, next sibling),
+// kept in per-thread buffers reused across calls; a trie has at most a few
+// hundred nodes, so the scan is short and the call allocates nothing once
+// warm.  The ancestor bitmask of a node is its parent's mask plus its own
+// bit, which is valid because a parent is always created before its
+// children.
 extern "C" int ooo_pack_tree(int32_t root_token, const int32_t* cand_tokens,
                              const int32_t* cand_offsets, int32_t n_cand, int32_t max_nodes,
                              int32_t max_depth, int32_t* token, int32_t* parent, int32_t* depth,
@@ -58,8 +60,12 @@ extern "C" int ooo_pack_tree(int32_t root_token, const int32_t* cand_tokens,
     for (int32_t t = 0; t < total; ++t)
       OOO_REQUIRE(cand_tokens[t] >= 0, OOO_ERR_INVALID, "negative token at position %d", t);
 
-    std::unordered_map<uint64_t, int32_t> child;  // (parent << 32 | token) -> node
-    child.reserve(2 * (size_t)max_nodes);
+    thread_local std::vector<int32_t> first_child, next_sibling;
+    if (first_child.size() < (size_t)max_nodes) {
+      first_child.resize(max_nodes);
+      next_sibling.resize(max_nodes);
+    }
+    first_child[0] = -1;
     int32_t n = 1;
     int32_t dropped = 0;
     token[0] = root_token;
@@ -76,10 +82,10 @@ extern "C" int ooo_pack_tree(int32_t root_token, const int32_t* cand_tokens,
           break;
         }
         const int32_t t = cand_tokens[a + pos];
-        const uint64_t key = ((uint64_t)(uint32_t)cur << 32) | (uint32_t)t;
-        auto it = child.find(key);
-        if (it != child.end()) {
-          cur = it->second;
+        int32_t ch = first_child[cur];
+        while (ch >= 0 && token[ch] != t) ch = next_sibling[ch];
+        if (ch >= 0) {
+          cur = ch;
           continue;
         }
         if (n >= max_nodes) {
@@ -94,7 +100,9 @@ extern "C" int ooo_pack_tree(int32_t root_token, const int32_t* cand_tokens,
         const uint64_t* prow = anc_mask + (size_t)cur * mask_words;
         for (int32_t w = 0; w < mask_words; ++w) row[w] = prow[w];
         row[node >> 6] |= 1ull << (node & 63);
-        child.emplace(key, node);
+        first_child[node] = -1;
+        next_sibling[node] = first_child[cur];  // newest first; order does not affect the trie
+        first_child[cur] = node;
         cur = node;
       }
     }

@@ -169,6 +169,39 @@ def pack_tree_into(root_token: int, cand_tokens: np.ndarray, cand_offsets: np.nd
     return n.value, trunc.value
 
 
+class StagedPacker:
+    """ooo_pack_tree bound to fixed output arrays (the per-step staging
+    buffer): their addresses are resolved once, so a call only marshals the
+    candidate arrays.  Returns (n_nodes, n_truncated)."""
+
+    _proto = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                              ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                              ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p)
+
+    def __init__(self, max_nodes: int, max_depth: int, token: np.ndarray, parent: np.ndarray, depth: np.ndarray,
+                 anc_mask: np.ndarray):
+        for a, nm, dt in ((token, "token", np.int32), (parent, "parent", np.int32), (depth, "depth", np.int32),
+                          (anc_mask, "anc_mask", np.uint64)):
+            if a.dtype != dt or not a.flags.c_contiguous or a.shape[0] < max_nodes:
+                raise ValueError(f"{nm} must be a C-contiguous {np.dtype(dt).name} array of >= {max_nodes} rows")
+        self._fn = self._proto(("ooo_pack_tree", lib()))
+        self._keep = (token, parent, depth, anc_mask)  # the addresses below stay valid
+        self._n, self._trunc = ctypes.c_int32(0), ctypes.c_int32(0)
+        W = 1 if anc_mask.ndim == 1 else int(anc_mask.shape[1])
+        self._fixed = (int(max_nodes), int(max_depth), token.ctypes.data, parent.ctypes.data, depth.ctypes.data,
+                       anc_mask.ctypes.data, W, ctypes.addressof(self._n), ctypes.addressof(self._trunc))
+
+    def __call__(self, root_token: int, cand_tokens: np.ndarray, cand_offsets: np.ndarray) -> tuple:
+        if cand_tokens.dtype != np.int32 or not cand_tokens.flags.c_contiguous:
+            cand_tokens = np.ascontiguousarray(cand_tokens, dtype=np.int32)
+        if cand_offsets.dtype != np.int32 or not cand_offsets.flags.c_contiguous:
+            cand_offsets = np.ascontiguousarray(cand_offsets, dtype=np.int32)
+        mn, md, t, p, d, m, W, n, tr = self._fixed
+        _check(self._fn(int(root_token), cand_tokens.ctypes.data if cand_tokens.size else None,
+                        cand_offsets.ctypes.data, cand_offsets.shape[0] - 1, mn, md, t, p, d, m, W, n, tr))
+        return self._n.value, self._trunc.value
+
+
 def hint_merge(bank: np.ndarray, eos_token: int, committed: np.ndarray, native_tokens: np.ndarray,
                native_offsets: np.ndarray, n_lanes: int, max_suffix: int = 7, max_len: int = 64) -> dict:
     """ooo_hint_merge on NumPy arrays: the merged lanes as CSR (tokens,

@@ -80,6 +80,8 @@ class VerifyRunner:
         self.n_nodes = 0
         self.n_truncated = 0
         self.packed = None
+        self._packer = ooo.StagedPacker(max_nodes, max_depth, self._h_token, self._h_parent, self._h_depth,
+                                        self._h_mask)
 
     # -- host ---------------------------------------------------------------
     def pack(self, root_token: int, cand_tokens: np.ndarray, cand_offsets: np.ndarray,
@@ -87,8 +89,7 @@ class VerifyRunner:
         """Pack the candidates straight into the pinned staging buffer.  With
         keep, also return copies of the trie arrays (the buffer is rewritten
         by the next pack); without, return None (the per-step path)."""
-        k, trunc = ooo.pack_tree_into(root_token, cand_tokens, cand_offsets, self.max_nodes, self.max_depth,
-                                      self._h_token, self._h_parent, self._h_depth, self._h_mask)
+        k, trunc = self._packer(root_token, cand_tokens, cand_offsets)
         self.n_nodes = k
         self.n_truncated = trunc
         self.packed = None
