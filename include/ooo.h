@@ -17,6 +17,16 @@
  *   ooo_kv_compact     move the accepted nodes' K/V rows into the committed
  *                      cache, directly after the prefix
  *
+ * The target decoder layer around the path (the target scores the tree in
+ * one forward pass, Section 4.5; Qwen3 targets, Section 5):
+ *
+ *   ooo_embed_rows     residual rows of the trie's tokens
+ *   ooo_rmsnorm        RMSNorm of residual rows (fp32 in, bf16 out)
+ *   ooo_linear         x W^T (+ y): the plain projections (hipBLASLt)
+ *   ooo_qk_norm_rope   per-head q/k norms, rotation at position P + depth,
+ *                      q out, node k/v into the layer's cache rows
+ *   ooo_swiglu         silu(gate) * up of the fused MLP projection
+ *
  * Conventions shared by every entry point
  *   - Return value: OOO_OK (0) or a negative ooo_status.  On error nothing has
  *     been enqueued and ooo_last_error() returns a message (thread-local,
@@ -263,6 +273,95 @@ int ooo_kv_compact(void* k_cache, void* v_cache, int32_t n_layers, int32_t n_kv_
                    int64_t cap, int32_t head_dim, ooo_dtype dt, int32_t prefix_len,
                    int32_t n_nodes, const int32_t* path, const int32_t* accept_len,
                    int32_t path_cap, void* stream);
+
+/*
+ * ooo_embed_rows - residual rows of the trie's tokens (the input of the
+ * target's first layer; Section 4.5: one forward pass over the tree).
+ *
+ * DEVICE pointers; asynchronous on `stream`.
+ *   table    [vocab][hidden_dim] bf16 embedding table
+ *   tokens   [n_nodes] int32 (the packed trie's tokens)
+ *   h        [n_nodes][hidden_dim] float32 output
+ * A token outside [0, vocab) gives a row of NaN.
+ * Errors: OOO_ERR_INVALID (null pointers, sizes < 1), OOO_ERR_HIP.
+ */
+int ooo_embed_rows(const void* table, const int32_t* tokens, int32_t n_nodes, int32_t hidden_dim,
+                   int32_t vocab, float* h, void* stream);
+
+/*
+ * ooo_rmsnorm - out = h / sqrt(mean(h^2) + eps) * weight per row (the
+ * target's pre-attention, pre-MLP and final norms; Section 5, Qwen3).
+ *
+ * DEVICE pointers; asynchronous on `stream`.
+ *   h        [n_rows][dim] float32 residual rows
+ *   weight   [dim] bf16
+ *   out      [n_rows][dim] bf16; must not alias h
+ * Errors: OOO_ERR_INVALID (null pointers, sizes < 1, eps < 0), OOO_ERR_HIP.
+ */
+int ooo_rmsnorm(const float* h, const void* weight, int32_t n_rows, int32_t dim, float eps, void* out,
+                void* stream);
+
+/*
+ * ooo_linear - y = x W^T, or y += x W^T with accumulate != 0 (the target's
+ * q/k/v, output and MLP projections; plain GEMMs run by hipBLASLt).
+ *
+ * DEVICE pointers; asynchronous on `stream`.
+ *   x        [n_rows][in_dim] bf16
+ *   weight   [out_dim][in_dim] bf16 (nn.Linear layout)
+ *   out      [n_rows][out_dim], float32 or bf16 (out_dt); read when
+ *            accumulate != 0; must not alias x or weight
+ *   workspace, ws_bytes   scratch for the GEMM (ooo_linear_workspace()
+ *            bytes is always enough; 0 bytes is allowed)
+ * float32 accumulation.  The first call for a new (n_rows, in_dim, out_dim,
+ * out_dt) chooses the GEMM algorithm on the host; calls inside a HIP graph
+ * capture should repeat shapes already used once.
+ * Errors: OOO_ERR_INVALID (null pointers, sizes < 1, unknown dtype),
+ * OOO_ERR_UNSUPPORTED (no algorithm within ws_bytes), OOO_ERR_HIP.
+ */
+size_t ooo_linear_workspace(void);
+int ooo_linear(const void* x, const void* weight, int32_t n_rows, int32_t in_dim, int32_t out_dim,
+               ooo_dtype out_dt, int32_t accumulate, void* out, void* workspace, size_t ws_bytes,
+               void* stream);
+
+/*
+ * ooo_qk_norm_rope - queries of the trie nodes and their keys/values in the
+ * cache (Section 4.5: one forward pass over the tree).  Node i takes the
+ * rotary position P + depth[i], the position sequential decoding of its own
+ * root path would give it; its key and value go to cache row P + i, where
+ * ooo_tree_attn reads them.
+ *
+ * DEVICE pointers; asynchronous on `stream`.
+ *   qkv       [n_nodes][(n_q_heads + 2 n_kv_heads) head_dim] bf16: the fused
+ *             projection, q heads, then k heads, then v heads
+ *   q_norm, k_norm   [head_dim] bf16 per-head RMSNorm weights of q and k
+ *             (Qwen3), or NULL for no norm
+ *   depth     [n_nodes] int32 (the packed trie's depths)
+ *   q_out     [n_nodes][n_q_heads][head_dim] bf16
+ *   k_cache, v_cache   one layer, [n_kv_heads][cap][head_dim] bf16; rows
+ *             P .. P + n_nodes - 1 are written
+ * Rotation: the pair (j, j + head_dim/2) turns by the angle
+ * (P + depth[i]) * rope_theta^(-2j/head_dim), computed in double precision.
+ * Norms in float32 with epsilon eps.
+ * Errors: OOO_ERR_INVALID (null pointers, sizes < 1, P + n_nodes > cap,
+ * rope_theta <= 0), OOO_ERR_UNSUPPORTED (head_dim other than 64 or 128),
+ * OOO_ERR_HIP.
+ */
+int ooo_qk_norm_rope(const void* qkv, const void* q_norm, const void* k_norm, float eps,
+                     const int32_t* depth, int32_t n_nodes, int32_t prefix_len, double rope_theta,
+                     int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, void* q_out,
+                     void* k_cache, void* v_cache, int64_t cap, void* stream);
+
+/*
+ * ooo_swiglu - out[n][j] = silu(g) * u with g = gate_up[n][j] and
+ * u = gate_up[n][intermediate + j] (the target's MLP activation; the fused
+ * projection holds the gate rows, then the up rows).
+ *
+ * DEVICE pointers; asynchronous on `stream`.
+ *   gate_up  [n_rows][2 intermediate] float32
+ *   out      [n_rows][intermediate] bf16
+ * Errors: OOO_ERR_INVALID (null pointers, sizes < 1), OOO_ERR_HIP.
+ */
+int ooo_swiglu(const float* gate_up, int32_t n_rows, int32_t intermediate, void* out, void* stream);
 
 #ifdef __cplusplus
 }

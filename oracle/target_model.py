@@ -98,8 +98,10 @@ def silu(x: np.ndarray) -> np.ndarray:
     return x / (1.0 + np.exp(-x))
 
 
-def embed(table: np.ndarray, tokens: Sequence[int]) -> np.ndarray:
-    return np.asarray(table, dtype=np.float64)[np.asarray(tokens, dtype=np.int64)]
+def embed(table, tokens: Sequence[int]) -> np.ndarray:
+    """Rows of the embedding table (widened after the lookup, so a table
+    object that widens on indexing can stand in for a large one)."""
+    return np.asarray(table[np.asarray(tokens, dtype=np.int64)], dtype=np.float64)
 
 
 # ----------------------------------------------------------------------------

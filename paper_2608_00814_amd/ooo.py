@@ -47,6 +47,13 @@ SIGNATURES = {
     "ooo_accept": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i32, _vp, _i32, _i32, _vp, _vp, _vp, _vp]),
     "ooo_kv_compact": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i64, _i32, ctypes.c_int, _i32, _i32, _vp, _vp,
                                       _i32, _vp]),
+    "ooo_embed_rows": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _vp, _vp]),
+    "ooo_rmsnorm": (ctypes.c_int, [_vp, _vp, _i32, _i32, ctypes.c_float, _vp, _vp]),
+    "ooo_linear_workspace": (_sz, []),
+    "ooo_linear": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, ctypes.c_int, _i32, _vp, _vp, _sz, _vp]),
+    "ooo_qk_norm_rope": (ctypes.c_int, [_vp, _vp, _vp, ctypes.c_float, _vp, _i32, _i32, ctypes.c_double, _i32,
+                                        _i32, _i32, _vp, _vp, _vp, _i64, _vp]),
+    "ooo_swiglu": (ctypes.c_int, [_vp, _i32, _i32, _vp, _vp]),
 }
 
 
@@ -317,3 +324,61 @@ def kv_compact(k_cache, v_cache, prefix_len: int, n_nodes: int, path, accept_len
     _check(lib().ooo_kv_compact(k_cache.data_ptr(), v_cache.data_ptr(), L, Hkv, cap, D, dtype_code(k_cache),
                                 prefix_len, n_nodes, path.data_ptr(), accept_len.data_ptr(), path.numel(),
                                 _stream(stream)))
+
+
+# ----------------------------------------------------------------------------
+# decoder layer around the path
+
+
+def embed_rows(table, tokens, n_nodes: int, h, stream=None) -> None:
+    """table [V][H] bf16; tokens [>= n_nodes] int32; h [>= n_nodes][H] float32."""
+    for t, nm in ((table, "table"), (tokens, "tokens"), (h, "h")):
+        _dev(t, nm)
+    V, H = table.shape
+    _check(lib().ooo_embed_rows(table.data_ptr(), tokens.data_ptr(), n_nodes, H, V, h.data_ptr(), _stream(stream)))
+
+
+def rmsnorm(h, weight, eps: float, out, n_rows: Optional[int] = None, stream=None) -> None:
+    """h [rows][dim] float32; weight [dim] bf16; out [rows][dim] bf16."""
+    for t, nm in ((h, "h"), (weight, "weight"), (out, "out")):
+        _dev(t, nm)
+    n = h.shape[0] if n_rows is None else n_rows
+    _check(lib().ooo_rmsnorm(h.data_ptr(), weight.data_ptr(), n, h.shape[-1], float(eps), out.data_ptr(),
+                             _stream(stream)))
+
+
+def linear_workspace() -> int:
+    return int(lib().ooo_linear_workspace())
+
+
+def linear(x, weight, out, n_rows: Optional[int] = None, accumulate: bool = False, workspace=None,
+           stream=None) -> None:
+    """out[:n] (+)= x[:n] @ weight.T with x bf16 [rows][in], weight bf16
+    [out][in], out float32 or bf16 [rows][out]."""
+    for t, nm in ((x, "x"), (weight, "weight"), (out, "out")):
+        _dev(t, nm)
+    n = x.shape[0] if n_rows is None else n_rows
+    O, K = weight.shape
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().ooo_linear(x.data_ptr(), weight.data_ptr(), n, K, O, dtype_code(out), int(bool(accumulate)),
+                            out.data_ptr(), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def qk_norm_rope(qkv, q_norm, k_norm, eps: float, depth, n_nodes: int, prefix_len: int, rope_theta: float,
+                 n_q_heads: int, n_kv_heads: int, q_out, k_cache, v_cache, stream=None) -> None:
+    """qkv [N][(Hq + 2 Hkv) D] bf16; q_norm/k_norm [D] bf16 or None; depth
+    [>= N] int32; q_out [N][Hq][D]; k_cache/v_cache one layer [Hkv][cap][D]."""
+    for t, nm in ((qkv, "qkv"), (depth, "depth"), (q_out, "q_out"), (k_cache, "k_cache"), (v_cache, "v_cache")):
+        _dev(t, nm)
+    _, cap, D = k_cache.shape
+    _check(lib().ooo_qk_norm_rope(qkv.data_ptr(), _ptr(q_norm), _ptr(k_norm), float(eps), depth.data_ptr(), n_nodes,
+                                  prefix_len, float(rope_theta), n_q_heads, n_kv_heads, D, q_out.data_ptr(),
+                                  k_cache.data_ptr(), v_cache.data_ptr(), cap, _stream(stream)))
+
+
+def swiglu(gate_up, out, n_rows: Optional[int] = None, stream=None) -> None:
+    """gate_up [rows][2 I] float32 (gate rows, then up rows) -> out [rows][I] bf16."""
+    _dev(gate_up, "gate_up")
+    _dev(out, "out")
+    n = gate_up.shape[0] if n_rows is None else n_rows
+    _check(lib().ooo_swiglu(gate_up.data_ptr(), n, out.shape[-1], out.data_ptr(), _stream(stream)))

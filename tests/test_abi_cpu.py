@@ -27,7 +27,7 @@ def declared_functions():
 
 def test_exports_match_header():
     names = declared_functions()
-    assert len(names) == 12
+    assert len(names) == 18
     assert set(names) == set(ooo.SIGNATURES)
     lib = ooo.lib()
     for n in names:
@@ -142,6 +142,35 @@ def test_pack_rejects_bad_arguments(kwargs):
     st = _call_pack(**kwargs)
     assert st == ooo.ERR_INVALID
     assert ooo.last_error() != ""
+
+
+def test_layer_entry_points_validate_on_host():
+    L = ooo.lib()
+    fake = ctypes.c_void_p(256)  # never dereferenced: every call below fails validation first
+    assert L.ooo_embed_rows(None, fake, 4, 64, 100, fake, None) == ooo.ERR_INVALID
+    assert L.ooo_embed_rows(fake, fake, 0, 64, 100, fake, None) == ooo.ERR_INVALID
+    assert L.ooo_rmsnorm(fake, None, 4, 64, 1e-6, fake, None) == ooo.ERR_INVALID
+    assert L.ooo_rmsnorm(fake, fake, 4, 64, -1.0, fake, None) == ooo.ERR_INVALID
+    assert L.ooo_linear(fake, fake, 0, 64, 64, ooo.BF16, 0, fake, None, 0, None) == ooo.ERR_INVALID
+    assert L.ooo_linear(None, fake, 4, 64, 64, ooo.BF16, 0, fake, None, 0, None) == ooo.ERR_INVALID
+    assert L.ooo_linear(fake, fake, 4, 64, 64, 7, 0, fake, None, 0, None) == ooo.ERR_INVALID
+    assert L.ooo_linear(fake, fake, 4, 64, 64, ooo.F32, 0, fake, None, 1024, None) == ooo.ERR_INVALID
+    args = dict(qkv=fake, qn=fake, kn=fake, eps=1e-6, depth=fake, N=4, P=10, theta=1e6, Hq=4, Hkv=2, D=128,
+                q=fake, kc=fake, vc=fake, cap=100)
+
+    def qk(**kw):
+        a = {**args, **kw}
+        return L.ooo_qk_norm_rope(a["qkv"], a["qn"], a["kn"], a["eps"], a["depth"], a["N"], a["P"], a["theta"],
+                                  a["Hq"], a["Hkv"], a["D"], a["q"], a["kc"], a["vc"], a["cap"], None)
+    assert qk(qkv=None) == ooo.ERR_INVALID
+    assert qk(depth=None) == ooo.ERR_INVALID
+    assert qk(P=97) == ooo.ERR_INVALID  # P + N > cap
+    assert qk(theta=0.0) == ooo.ERR_INVALID
+    assert qk(N=0) == ooo.ERR_INVALID
+    assert qk(D=96) == ooo.ERR_UNSUPPORTED
+    assert L.ooo_swiglu(None, 4, 64, fake, None) == ooo.ERR_INVALID
+    assert L.ooo_swiglu(fake, 4, 0, fake, None) == ooo.ERR_INVALID
+    assert ooo.linear_workspace() > 0
 
 
 def test_device_entry_points_validate_on_host():

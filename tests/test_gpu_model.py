@@ -1,0 +1,224 @@
+"""Decoder layers around the verification path on the GPU against the CPU
+reference (``oracle/target_model.py``), through the C ABI.
+
+Per-kernel parity (norms, projections, the rotation at P + depth with the
+cache writes, the MLP activation, embedding rows) and whole verify steps of
+a 2-layer model and of 2 layers at the Qwen3-8B decoder's sizes.  Float
+outputs are compared per row (max abs error / max abs reference <= 1e-2);
+greedy tokens, the accepted length, the path and the bonus token exactly on
+nodes whose reference margin is at least 1e-2.
+"""
+
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import gpu_harness as gh
+from oracle import target_model as om
+from oracle import tree_verify as ov
+from paper_2608_00814_amd import model_workload as mw
+from paper_2608_00814_amd import ooo
+from paper_2608_00814_amd import workload as wl
+from paper_2608_00814_amd.model import ModelRunner
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+TOL = gh.ATTN_TOL
+f64 = wl.bf16_to_f64
+
+
+def _bits(rs, shape, std=1.0):
+    return wl.to_bf16_bits(rs.normal(0, std, size=shape).astype(np.float32))
+
+
+def _dev_bf16(bits):
+    return gh.to_dev(bits, "bf16", DEV)
+
+
+def _host_f64(t):
+    return f64(gh.to_host(t, "bf16"))
+
+
+@pytest.mark.parametrize("N,H", [(1, 64), (37, 4096), (64, 5120)])
+def test_rmsnorm(N, H):
+    print(f"case rmsnorm N={N} H={H}", flush=True)
+    rs = np.random.default_rng(N + H)
+    h = (rs.normal(0, 3, size=(N, H))).astype(np.float32)
+    w = _bits(rs, H, 0.3)
+    out = torch.empty(N, H, dtype=torch.bfloat16, device=DEV)
+    ooo.rmsnorm(torch.from_numpy(h).to(DEV), _dev_bf16(w), 1e-6, out)
+    ref = om.rmsnorm(h.astype(np.float64), f64(w), 1e-6)
+    assert gh.row_rel_err(_host_f64(out), ref) <= TOL
+
+
+@pytest.mark.parametrize("N,K,O", [(64, 4096, 6144), (64, 4096, 4096), (37, 4096, 24576), (64, 12288, 4096),
+                                   (1, 256, 1152), (5, 512, 256)])
+def test_linear(N, K, O):
+    print(f"case linear N={N} K={K} O={O}", flush=True)
+    rs = np.random.default_rng(N + K + O)
+    x, w = _bits(rs, (N, K)), _bits(rs, (O, K), 0.02)
+    xd, wd = _dev_bf16(x), _dev_bf16(w)
+    ref = f64(x) @ f64(w).T
+    ws = torch.empty(ooo.linear_workspace(), dtype=torch.uint8, device=DEV)
+    y32 = torch.empty(N, O, dtype=torch.float32, device=DEV)
+    ooo.linear(xd, wd, y32, workspace=ws)
+    assert gh.row_rel_err(y32.double().cpu().numpy(), ref) <= 1e-4
+    y16 = torch.empty(N, O, dtype=torch.bfloat16, device=DEV)
+    ooo.linear(xd, wd, y16, workspace=ws)
+    assert gh.row_rel_err(_host_f64(y16), ref) <= TOL
+    base = rs.normal(size=(N, O)).astype(np.float32)
+    acc = torch.from_numpy(base).to(DEV)
+    ooo.linear(xd, wd, acc, accumulate=True, workspace=ws)
+    assert gh.row_rel_err(acc.double().cpu().numpy(), ref + base) <= 1e-4
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("N,Hq,Hkv,D,P,norm", [(64, 32, 8, 128, 4096, True), (33, 4, 2, 64, 100, True),
+                                                (7, 40, 8, 128, 8192, False), (1, 2, 1, 64, 0, True)])
+def test_qk_norm_rope(N, Hq, Hkv, D, P, norm):
+    """Queries, and the node keys/values in the cache rows P .. P + N - 1,
+    match the reference norms and rotation at positions P + depth; every
+    other cache row is left untouched."""
+    print(f"case qk_norm_rope N={N} Hq={Hq} Hkv={Hkv} D={D} P={P} norm={norm}", flush=True)
+    rs = np.random.default_rng(N + Hq + D + P)
+    theta = 1.0e6
+    qkv = _bits(rs, (N, (Hq + 2 * Hkv) * D))
+    qn = kn = None
+    if norm:
+        qn = wl.to_bf16_bits(1.0 + 0.2 * rs.normal(size=D).astype(np.float32))
+        kn = wl.to_bf16_bits(1.0 + 0.2 * rs.normal(size=D).astype(np.float32))
+    depth = rs.integers(0, 50, size=N).astype(np.int32)
+    depth[0] = 0
+    cap = P + N + 5
+    sentinel = np.uint16(0x3F80)  # 1.0
+    kc = torch.full((Hkv, cap, D), 1.0, dtype=torch.bfloat16, device=DEV)
+    vc = torch.full((Hkv, cap, D), 1.0, dtype=torch.bfloat16, device=DEV)
+    q_out = torch.empty(N, Hq, D, dtype=torch.bfloat16, device=DEV)
+    ooo.qk_norm_rope(_dev_bf16(qkv), _dev_bf16(qn) if norm else None, _dev_bf16(kn) if norm else None, 1e-6,
+                     torch.from_numpy(depth).to(DEV), N, P, theta, Hq, Hkv, q_out, kc, vc)
+    q = f64(qkv[:, :Hq * D]).reshape(N, Hq, D)
+    k = f64(qkv[:, Hq * D:(Hq + Hkv) * D]).reshape(N, Hkv, D)
+    if norm:
+        q, k = om.rmsnorm(q, f64(qn), 1e-6), om.rmsnorm(k, f64(kn), 1e-6)
+    pos = P + depth.astype(np.int64)
+    q_ref, k_ref = om.rope(q, pos, theta), om.rope(k, pos, theta)
+    assert gh.row_rel_err(_host_f64(q_out), q_ref) <= TOL
+    kh, vh = gh.to_host(kc, "bf16"), gh.to_host(vc, "bf16")
+    assert gh.row_rel_err(f64(kh[:, P:P + N].transpose(1, 0, 2)), k_ref) <= TOL
+    assert np.array_equal(vh[:, P:P + N].transpose(1, 0, 2).reshape(N, -1), qkv[:, (Hq + Hkv) * D:])
+    for arr in (kh, vh):
+        assert (arr[:, :P] == sentinel).all() and (arr[:, P + N:] == sentinel).all()
+
+
+def test_swiglu_and_embedding():
+    print("case swiglu and embedding rows", flush=True)
+    rs = np.random.default_rng(5)
+    N, I, V, H = 19, 3072, 500, 1024
+    gu = (rs.normal(0, 4, size=(N, 2 * I))).astype(np.float32)
+    out = torch.empty(N, I, dtype=torch.bfloat16, device=DEV)
+    ooo.swiglu(torch.from_numpy(gu).to(DEV), out)
+    g, u = gu[:, :I].astype(np.float64), gu[:, I:].astype(np.float64)
+    assert gh.row_rel_err(_host_f64(out), om.silu(g) * u) <= TOL
+    table = _bits(rs, (V, H))
+    toks = rs.integers(0, V, size=N).astype(np.int32)
+    h = torch.empty(N, H, dtype=torch.float32, device=DEV)
+    ooo.embed_rows(_dev_bf16(table), torch.from_numpy(toks).to(DEV), N, h)
+    assert np.array_equal(h.cpu().numpy().astype(np.float64), f64(table[toks]))
+
+
+# ----------------------------------------------------------------------------
+# whole verify steps of the model
+
+
+class _Widen:
+    """A bf16 table that widens the rows it is indexed with."""
+
+    def __init__(self, bits):
+        self.bits = bits
+        self.shape = bits.shape
+
+    def __getitem__(self, idx):
+        return f64(self.bits[idx])
+
+
+def _model(cfg, seed, n_layers):
+    lws = [mw.layer_weights(cfg, seed, l) for l in range(n_layers)]
+    emb, fin, lm = mw.embedding(cfg, seed), mw.final_norm(cfg, seed), mw.lm_head(cfg, seed)
+    ref_layers = [om.LayerWeights(**{k: f64(v) for k, v in lw.items()}) for lw in lws]
+    shp = om.ModelShape(hidden=cfg.hidden, n_q_heads=cfg.n_q_heads, n_kv_heads=cfg.n_kv_heads,
+                        head_dim=cfg.head_dim, intermediate=cfg.intermediate, rope_theta=cfg.rope_theta, eps=cfg.eps)
+    return lws, emb, fin, lm, ref_layers, shp
+
+
+def _greedy_chain(cfg, shp, ref_layers, emb, fin, lm, kcs, vcs, root, P, d):
+    """The reference's own greedy continuation of length d + 1 after root
+    (teacher-forced chains of growing length; caches are copied)."""
+    chain = []
+    for _ in range(d + 1):
+        tree = ov.pack_tree(root, [chain] if chain else [], 64, 64)
+        fw = om.forward_tree(tree["token"], tree["parent"], tree["depth"], P, _Widen(emb), ref_layers, f64(fin),
+                             shp, [k.copy() for k in kcs], [v.copy() for v in vcs])
+        g = ov.greedy_tokens(ov.lm_head_logits(fw["x"], _Widen(lm)))
+        chain.append(int(g["ids"][-1]))
+    return chain
+
+
+@pytest.mark.parametrize("name,n_layers,depth", [("small-model", 2, 5), ("qwen3-8b-model", 2, 2)])
+def test_model_verify_step(name, n_layers, depth):
+    """Pack, all layers, LM head, accept and compact on the GPU against the
+    reference step, with candidates that contain the reference's own greedy
+    continuation for `depth` tokens (so exactly that many are accepted)."""
+    print(f"case model verify step {name} layers={n_layers} depth={depth}", flush=True)
+    base = mw.MODEL_CONFIGS[name]
+    import dataclasses
+    cfg = dataclasses.replace(base, n_layers=n_layers)
+    seed = 3
+    lws, emb, fin, lm, ref_layers, shp = _model(cfg, seed, n_layers)
+    P = cfg.prefix_len
+    kv = [mw.prefix_kv(cfg, seed, l) for l in range(n_layers)]
+    kcs = [f64(k) for k, _ in kv]
+    vcs = [f64(v) for _, v in kv]
+    toks = mw.random_tokens(cfg, seed, 40)
+    root = toks[0]
+    chain = _greedy_chain(cfg, shp, ref_layers, emb, fin, lm, kcs, vcs, root, P, depth)
+    wrong = (chain[depth] + 1) % cfg.vocab
+    cands = [chain[:depth] + [wrong] + toks[1:4], toks[4:9], chain[:1] + toks[9:12], toks[12:15]]
+    ref = om.verify_step(root, cands, cfg.max_nodes, cfg.max_depth, P, _Widen(emb), ref_layers, f64(fin), _Widen(lm),
+                         shp, kcs, vcs)
+    assert ref["L"] == depth
+    # GPU
+    runner = ModelRunner(cfg, lws, emb, fin, lm, DEV)
+    kc = torch.stack([_dev_bf16(k) for k, _ in kv])
+    vc = torch.stack([_dev_bf16(v) for _, v in kv])
+    offs = np.zeros(len(cands) + 1, np.int32)
+    for i, c in enumerate(cands):
+        offs[i + 1] = offs[i] + len(c)
+    flat = np.array([t for c in cands for t in c], np.int32)
+    packed = runner.pack(root, flat, offs)
+    N = packed["n_nodes"]
+    assert N == ref["tree"]["n_nodes"] and np.array_equal(packed["token"], ref["tree"]["token"])
+    logits = torch.empty(N, cfg.vocab, dtype=torch.float32, device=DEV)
+    runner.device_step(kc, vc, P, logits=logits)
+    torch.cuda.synchronize()
+    res = runner.result()
+    x_gpu = _host_f64(runner.xf[:N])
+    assert gh.row_rel_err(x_gpu, ref["x"]) <= TOL
+    ids = runner.vr.ids[:N].cpu().numpy()
+    ok = ref["margin"] >= 1e-2
+    assert ok[ref["path"]].all()
+    assert np.array_equal(ids[ok], ref["ids"][ok])
+    assert res.L == ref["L"] and res.bonus == ref["bonus"]
+    assert np.array_equal(res.path, ref["path"])
+    # the cache: prefix rows unchanged, rows P .. P + L hold the accepted
+    # nodes' keys/values (bf16 rounding of the reference)
+    for l in range(n_layers):
+        kh = gh.to_host(kc[l], "bf16")
+        vh = gh.to_host(vc[l], "bf16")
+        assert np.array_equal(kh[:, :P], kv[l][0][:, :P]) and np.array_equal(vh[:, :P], kv[l][1][:, :P])
+        rows = slice(P, P + ref["L"] + 1)
+        assert gh.row_rel_err(f64(kh[:, rows]), kcs[l][:, rows]) <= TOL
+        assert gh.row_rel_err(f64(vh[:, rows]), vcs[l][:, rows]) <= TOL
