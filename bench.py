@@ -150,6 +150,250 @@ def cpu_baseline(cfg, seconds: float):
                       f"with {threads} BLAS threads"}
 
 
+MODEL_METRIC = "full-model verify steps/s, Qwen3-8B decoder (36 layers, random weights), 64-node trie, 4k ctx"
+
+
+def model_cpu_baseline(mcfg, seconds: float):
+    """The decoder reference on a bounded sample of the full-model step: one
+    full-size layer over the step's trie (repeated until about ``seconds``
+    have passed) plus one LM head and accept; the step time is scaled to all
+    layers."""
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    from oracle import target_model as om
+    from oracle import tree_verify as ov
+    from paper_2608_00814_amd import model_workload as mw
+    from paper_2608_00814_amd import workload as wl
+    f64 = wl.bf16_to_f64
+    seed = 0
+    pcfg = wl.CONFIGS["qwen3-8b"]
+    cands = wl.candidates_for(pcfg, seed, 0)
+    tree = ov.pack_tree(cands.root_token, cands.seqs, mcfg.max_nodes, mcfg.max_depth)
+    lw = om.LayerWeights(**{k: f64(v) for k, v in mw.layer_weights(mcfg, seed, 0).items()})
+    shp = om.ModelShape(hidden=mcfg.hidden, n_q_heads=mcfg.n_q_heads, n_kv_heads=mcfg.n_kv_heads,
+                        head_dim=mcfg.head_dim, intermediate=mcfg.intermediate, rope_theta=mcfg.rope_theta,
+                        eps=mcfg.eps)
+    k, v = mw.prefix_kv(mcfg, seed, 0)
+    kc, vc = f64(k), f64(v)
+    emb = mw.embedding(mcfg, seed)
+    h = f64(emb[np.asarray(tree["token"])])
+    del emb
+    reps = 0
+    t0 = time.perf_counter()
+    while True:
+        out = om.decoder_layer(h, lw, shp, kc, vc, mcfg.prefix_len, tree["parent"], tree["depth"])
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    t_layer = el / reps
+    lm = mw.lm_head(mcfg, seed)
+    t1 = time.perf_counter()
+    x = om.rmsnorm(out["h"], f64(mw.final_norm(mcfg, seed)), mcfg.eps)
+    g = ov.greedy_tokens(ov.lm_head_logits(x, _Widen(lm)))
+    ov.accept_walk(tree["token"], tree["parent"], g["ids"])
+    t_head = time.perf_counter() - t1
+    step = mcfg.n_layers * t_layer + t_head
+    return {"value": 1.0 / step, "unit": "verify steps/s", "cores": threads, "kind": "oracle",
+            "sample": f"{reps} full-size decoder layer(s) over the step's {tree['n_nodes']}-node trie "
+                      f"({t_layer:.2f} s each) plus one LM head and accept ({t_head:.2f} s) in fp64 NumPy, "
+                      f"scaled to {mcfg.n_layers} layers, on {platform.processor() or 'host'} with {threads} BLAS "
+                      f"threads"}
+
+
+class _Widen:
+    """bf16 table widened to float64 on indexing (row chunks of the LM head)."""
+
+    def __init__(self, bits):
+        self.bits, self.shape = bits, bits.shape
+
+    def __getitem__(self, idx):
+        from paper_2608_00814_amd import workload as wl
+        return wl.bf16_to_f64(self.bits[idx])
+
+
+def bench_model(args):
+    """Full verify steps of a Qwen3-8B-shaped decoder (random weights): the
+    decoder layers around the path, LM head, accept, compact."""
+    import torch
+
+    from paper_2608_00814_amd import model_workload as mw
+    from paper_2608_00814_amd import ooo
+    from paper_2608_00814_amd import workload as wl
+    from paper_2608_00814_amd.model import ModelRunner
+
+    ooo.lib()
+    mcfg = mw.MODEL_CONFIGS[args.workload]
+    dev = torch.device("cuda:0")
+    P = mcfg.prefix_len
+    t_setup = time.time()
+    seed = 0
+    layers = (mw.layer_weights(mcfg, seed, l) for l in range(mcfg.n_layers))  # uploaded one at a time
+    runner = ModelRunner(mcfg, layers, mw.embedding(mcfg, seed), mw.final_norm(mcfg, seed), mw.lm_head(mcfg, seed),
+                         dev)
+    shp = (mcfg.n_layers, mcfg.n_kv_heads, mcfg.cap, mcfg.head_dim)
+    k_cache = torch.empty(shp, dtype=torch.bfloat16, device=dev)
+    v_cache = torch.empty(shp, dtype=torch.bfloat16, device=dev)
+    for l in range(mcfg.n_layers):
+        k, v = mw.prefix_kv(mcfg, seed, l)
+        k_cache[l].copy_(torch.from_numpy(k.view(np.int16)).view(torch.bfloat16))
+        v_cache[l].copy_(torch.from_numpy(v.view(np.int16)).view(torch.bfloat16))
+    stream = torch.cuda.Stream()
+    pcfg = wl.CONFIGS["qwen3-8b"]
+    with torch.cuda.stream(stream):
+        # the model's own greedy continuation of the root (planted into each
+        # step's first candidate, to a depth drawn like the path workload's)
+        root = wl.candidates_for(pcfg, seed, 0).root_token
+        rs = np.random.default_rng(1)
+
+        def lanes(c, first):
+            # the path workload's trie shape with `first` as its first lane
+            # (the hint): the other lanes' prefixes shared with the hint follow
+            hint = list(c.seqs[0])
+            seqs = [first]
+            for q in c.seqs[1:]:
+                m = 0
+                while m < min(len(q), len(hint)) and q[m] == hint[m]:
+                    m += 1
+                seqs.append(first[:m] + list(q[m:]))
+            offs = np.zeros(len(seqs) + 1, np.int32)
+            for i, q in enumerate(seqs):
+                offs[i + 1] = offs[i] + len(q)
+            return np.array([t for q in seqs for t in q], np.int32), offs
+
+        # the model's own greedy continuation of the root, built in tries of
+        # the same shape as the timed steps (so every row is computed exactly
+        # as it will be there): the depth-k node of the first lane is node k
+        c0 = wl.candidates_for(pcfg, 0, 0)
+        lane_len = len(c0.seqs[0])
+        filler = [int(t) for t in rs.integers(0, mcfg.vocab, size=lane_len)]
+        chain = []
+        for k in range(lane_len + 1):
+            runner.pack(root, *lanes(c0, chain + filler[k:]), keep=False)
+            runner.device_step(k_cache, v_cache, P, compact=False)
+            stream.synchronize()
+            chain.append(int(runner.vr.ids[k].item()))
+        # variants: the greedy chain up to depth d, a wrong token, fresh tokens
+        n_variants = 4
+        cand_sets, depths = [], []
+        for s in range(n_variants):
+            d = int(rs.integers(4, min(mcfg.max_depth, lane_len) + 1))
+            first = chain[:d] + [(chain[d] + 1) % mcfg.vocab]
+            first += [int(t) for t in rs.integers(0, mcfg.vocab, size=lane_len - len(first))]
+            cand_sets.append(lanes(c0, first))
+            depths.append(d)
+        sizes = {runner.pack(root, *cs, keep=False) or runner.vr.n_nodes for cs in cand_sets}
+        if len(sizes) != 1:
+            raise RuntimeError(f"candidate variants give different trie sizes {sorted(sizes)}")
+        # eager warm-up (GEMM plans), then one graph for the device step
+        runner.pack(root, *cand_sets[0], keep=False)
+        runner.device_step(k_cache, v_cache, P)
+        stream.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=stream):
+            runner.device_step(k_cache, v_cache, P)
+        stream.synchronize()
+    setup_s = time.time() - t_setup
+
+    # per-phase breakdown on eager steps (outside the timed steps)
+    with torch.cuda.stream(stream):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        cfg, vr = mcfg, runner.vr
+        phase = {"projections_us": 0.0, "attention_us": 0.0, "other_us": 0.0}
+        reps = 3
+        for _ in range(reps):
+            runner.pack(root, *cand_sets[0], keep=False)
+            vr.upload_tree()
+            N = vr.n_nodes
+            ooo.embed_rows(runner.emb, vr.token, N, runner.h)
+            for l, w in enumerate(runner.layers):
+                ev[0].record(stream)
+                ooo.rmsnorm(runner.h, w["in_norm"], cfg.eps, runner.x, n_rows=N)
+                ev[1].record(stream)
+                ooo.linear(runner.x, w["w_qkv"], runner.qkv, n_rows=N, workspace=runner.lin_ws)
+                ev[2].record(stream)
+                ooo.qk_norm_rope(runner.qkv, w["q_norm"], w["k_norm"], cfg.eps, vr.depth, N, P, cfg.rope_theta,
+                                 cfg.n_q_heads, cfg.n_kv_heads, runner.q, k_cache[l], v_cache[l])
+                vr.attention(l, runner.q, k_cache[l], v_cache[l], P)
+                ev[3].record(stream)
+                stream.synchronize()
+                phase["other_us"] += 1e3 * ev[0].elapsed_time(ev[1])
+                phase["projections_us"] += 1e3 * ev[1].elapsed_time(ev[2])
+                phase["attention_us"] += 1e3 * ev[2].elapsed_time(ev[3])  # includes the q/k norms and rotation
+                o = vr.out[l].view(cfg.max_nodes, cfg.n_q_heads * cfg.head_dim)
+                ev[0].record(stream)
+                ooo.linear(o, w["w_o"], runner.h, n_rows=N, accumulate=True, workspace=runner.lin_ws)
+                ev[1].record(stream)
+                ooo.rmsnorm(runner.h, w["post_norm"], cfg.eps, runner.x, n_rows=N)
+                ev[2].record(stream)
+                ooo.linear(runner.x, w["w_gu"], runner.gu, n_rows=N, workspace=runner.lin_ws)
+                ooo.swiglu(runner.gu, runner.act, n_rows=N)
+                ooo.linear(runner.act, w["w_down"], runner.h, n_rows=N, accumulate=True, workspace=runner.lin_ws)
+                ev[3].record(stream)
+                stream.synchronize()
+                phase["projections_us"] += 1e3 * (ev[0].elapsed_time(ev[1]) + ev[2].elapsed_time(ev[3]))
+                phase["other_us"] += 1e3 * ev[1].elapsed_time(ev[2])
+        phase = {k: round(v / reps, 1) for k, v in phase.items()}
+
+        Ls = []
+        for i in range(args.warmup):
+            runner.pack(root, *cand_sets[i % n_variants], keep=False)
+            graph.replay()
+            stream.synchronize()
+            runner.result()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            runner.pack(root, *cand_sets[i % n_variants], keep=False)
+            graph.replay()
+            stream.synchronize()
+            Ls.append(runner.result().L)
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+    planted = [depths[i % n_variants] for i in range(args.steps)]
+    if Ls != planted:
+        print(f"note: {sum(a != b for a, b in zip(Ls, planted))} of {args.steps} steps accepted a different "
+              f"length than planted", file=sys.stderr)
+    w_bytes = mcfg.weight_bytes()
+    proj_gbs = w_bytes / (phase["projections_us"] * 1e-6) / 1e9
+    step_s = elapsed / args.steps
+    out = {
+        "metric": MODEL_METRIC,
+        "value": round(args.steps / elapsed, 2),
+        "unit": "verify steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(1e3 * step_s, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (random weights; each step's first candidate is the model's own greedy continuation)",
+        "config": {"workload": f"{mcfg.name}: {mcfg.description}", "n_layers": mcfg.n_layers, "hidden": mcfg.hidden,
+                   "q_heads": mcfg.n_q_heads, "kv_heads": mcfg.n_kv_heads, "head_dim": mcfg.head_dim,
+                   "intermediate": mcfg.intermediate, "vocab": mcfg.vocab, "prefix_len": P,
+                   "trie_nodes": int(runner.vr.n_nodes), "launch": "one hip-graph per step"},
+        "tokens_per_s": round(float(np.sum(np.array(Ls) + 1)) / elapsed, 1),
+        "mean_accepted_plus_bonus": round(float(np.mean(np.array(Ls) + 1)), 3),
+        "phase_us_eager": phase,
+        "roofline": {"bound": "hbm", "kernel": "projections (ooo_linear: qkv, o, gate+up, down over all layers)",
+                     "achieved": round(proj_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(proj_gbs / HBM_PEAK_GBS, 4), "traffic": None, "bytes_per_launch": w_bytes,
+                     "us_per_launch": phase["projections_us"]},
+        "step_weight_gbs": round(w_bytes / step_s / 1e9, 1),
+        "setup_s": round(setup_s, 1),
+    }
+    if not args.no_cpu_baseline:
+        del k_cache, v_cache, runner
+        torch.cuda.empty_cache()
+        out["cpu_baseline"] = model_cpu_baseline(mcfg, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -166,6 +410,11 @@ def main():
         print(f"bench.py measures one GPU only (asked for {args.gpus}); the path runs on a single MI355X.",
               file=sys.stderr)
         sys.exit(2)
+
+    from paper_2608_00814_amd import model_workload as mw
+    if args.workload in mw.MODEL_CONFIGS:
+        bench_model(args)
+        return
 
     import torch
 
