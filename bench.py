@@ -313,7 +313,7 @@ def bench_model(args):
                 ev[0].record(stream)
                 ooo.rmsnorm(runner.h, w["in_norm"], cfg.eps, runner.x, n_rows=N)
                 ev[1].record(stream)
-                ooo.linear(runner.x, w["w_qkv"], runner.qkv, n_rows=N, workspace=runner.lin_ws)
+                ooo.linear(runner.x, w["w_qkv"], runner.qkv, ooo.EPI_STORE_BF16, runner.lin_ws, n_rows=N)
                 ev[2].record(stream)
                 ooo.qk_norm_rope(runner.qkv, w["q_norm"], w["k_norm"], cfg.eps, vr.depth, N, P, cfg.rope_theta,
                                  cfg.n_q_heads, cfg.n_kv_heads, runner.q, k_cache[l], v_cache[l])
@@ -325,13 +325,12 @@ def bench_model(args):
                 phase["attention_us"] += 1e3 * ev[2].elapsed_time(ev[3])  # includes the q/k norms and rotation
                 o = vr.out[l].view(cfg.max_nodes, cfg.n_q_heads * cfg.head_dim)
                 ev[0].record(stream)
-                ooo.linear(o, w["w_o"], runner.h, n_rows=N, accumulate=True, workspace=runner.lin_ws)
+                ooo.linear(o, w["w_o"], runner.h, ooo.EPI_ADD_F32, runner.lin_ws, n_rows=N)
                 ev[1].record(stream)
                 ooo.rmsnorm(runner.h, w["post_norm"], cfg.eps, runner.x, n_rows=N)
                 ev[2].record(stream)
-                ooo.linear(runner.x, w["w_gu"], runner.gu, n_rows=N, workspace=runner.lin_ws)
-                ooo.swiglu(runner.gu, runner.act, n_rows=N)
-                ooo.linear(runner.act, w["w_down"], runner.h, n_rows=N, accumulate=True, workspace=runner.lin_ws)
+                ooo.linear(runner.x, w["w_gu"], runner.act, ooo.EPI_SWIGLU_BF16, runner.lin_ws, n_rows=N)
+                ooo.linear(runner.act, w["w_down"], runner.h, ooo.EPI_ADD_F32, runner.lin_ws, n_rows=N)
                 ev[3].record(stream)
                 stream.synchronize()
                 phase["projections_us"] += 1e3 * (ev[0].elapsed_time(ev[1]) + ev[2].elapsed_time(ev[3]))
@@ -380,7 +379,7 @@ def bench_model(args):
         "tokens_per_s": round(float(np.sum(np.array(Ls) + 1)) / elapsed, 1),
         "mean_accepted_plus_bonus": round(float(np.mean(np.array(Ls) + 1)), 3),
         "phase_us_eager": phase,
-        "roofline": {"bound": "hbm", "kernel": "projections (ooo_linear: qkv, o, gate+up, down over all layers)",
+        "roofline": {"bound": "hbm", "kernel": "projections (ooo_linear: qkv, o, gate+up, down over all layers; stream + reduce kernels)",
                      "achieved": round(proj_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(proj_gbs / HBM_PEAK_GBS, 4), "traffic": None, "bytes_per_launch": w_bytes,
                      "us_per_launch": phase["projections_us"]},

@@ -22,7 +22,8 @@
  *
  *   ooo_embed_rows     residual rows of the trie's tokens
  *   ooo_rmsnorm        RMSNorm of residual rows (fp32 in, bf16 out)
- *   ooo_linear         x W^T (+ y): the plain projections (hipBLASLt)
+ *   ooo_linear         x W^T with a fused epilogue: the projections
+ *                      (ooo_linear_pack lays a weight out for streaming)
  *   ooo_qk_norm_rope   per-head q/k norms, rotation at position P + depth,
  *                      q out, node k/v into the layer's cache rows
  *   ooo_swiglu         silu(gate) * up of the fused MLP projection
@@ -302,25 +303,41 @@ int ooo_rmsnorm(const float* h, const void* weight, int32_t n_rows, int32_t dim,
                 void* stream);
 
 /*
- * ooo_linear - y = x W^T, or y += x W^T with accumulate != 0 (the target's
- * q/k/v, output and MLP projections; plain GEMMs run by hipBLASLt).
+ * ooo_linear - the target's projections (q/k/v, output, gate/up, down) over
+ * the trie's rows: y = x W^T, bf16 operands, float32 accumulation, with the
+ * epilogue fused (Section 4.5: one forward pass over the tree; Section 5:
+ * Qwen3 targets).
  *
  * DEVICE pointers; asynchronous on `stream`.
- *   x        [n_rows][in_dim] bf16
- *   weight   [out_dim][in_dim] bf16 (nn.Linear layout)
- *   out      [n_rows][out_dim], float32 or bf16 (out_dt); read when
- *            accumulate != 0; must not alias x or weight
- *   workspace, ws_bytes   scratch for the GEMM (ooo_linear_workspace()
- *            bytes is always enough; 0 bytes is allowed)
- * float32 accumulation.  The first call for a new (n_rows, in_dim, out_dim,
- * out_dt) chooses the GEMM algorithm on the host; calls inside a HIP graph
- * capture should repeat shapes already used once.
- * Errors: OOO_ERR_INVALID (null pointers, sizes < 1, unknown dtype),
- * OOO_ERR_UNSUPPORTED (no algorithm within ws_bytes), OOO_ERR_HIP.
+ *   x        [n_rows][in_dim] bf16, n_rows <= 256, in_dim % 64 == 0
+ *   weight   [out_dim][in_dim] bf16 (nn.Linear layout, OOO_W_ROWS), or its
+ *            ooo_linear_pack layout (OOO_W_PACKED, the fast path)
+ *   out      [n_rows][out_dim] float32 (OOO_EPI_STORE_F32: y; OOO_EPI_ADD_F32:
+ *            out += y, e.g. the residual rows) or bf16 (OOO_EPI_STORE_BF16:
+ *            y); OOO_EPI_SWIGLU_BF16: weight holds the gate rows then the up
+ *            rows (out_dim = 2 I, I % 128 == 0) and out [n_rows][I] bf16 gets
+ *            silu(gate) * up.  out must not alias x or weight.
+ *   workspace, ws_bytes   ooo_linear_workspace(n_rows, in_dim, out_dim)
+ *            bytes of partial sums
+ * Deterministic: partial sums are added in a fixed order (no atomics).
+ * Errors: OOO_ERR_INVALID (null pointers, sizes < 1, unknown layout or
+ * epilogue), OOO_ERR_UNSUPPORTED (in_dim % 64, n_rows > 256, SwiGLU with
+ * out_dim % 256), OOO_ERR_CAPACITY (workspace too small), OOO_ERR_HIP.
  */
-size_t ooo_linear_workspace(void);
+typedef enum {
+  OOO_EPI_STORE_F32 = 0,
+  OOO_EPI_STORE_BF16 = 1,
+  OOO_EPI_ADD_F32 = 2,
+  OOO_EPI_SWIGLU_BF16 = 3
+} ooo_epilogue;
+size_t ooo_linear_workspace(int32_t n_rows, int32_t in_dim, int32_t out_dim);
+size_t ooo_linear_packed_bytes(int32_t out_dim, int32_t in_dim);
+/* One-time re-layout of a [out_dim][in_dim] bf16 weight into 16 KiB blocks
+ * of 128 rows x 64 columns (the layout of ooo_lmhead_pack); same errors. */
+int ooo_linear_pack(const void* weight, int32_t out_dim, int32_t in_dim, void* packed, size_t packed_bytes,
+                    void* stream);
 int ooo_linear(const void* x, const void* weight, int32_t n_rows, int32_t in_dim, int32_t out_dim,
-               ooo_dtype out_dt, int32_t accumulate, void* out, void* workspace, size_t ws_bytes,
+               int32_t weight_layout, ooo_epilogue epilogue, void* out, void* workspace, size_t ws_bytes,
                void* stream);
 
 /*

@@ -21,7 +21,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libooo.so")
 
-HIP_SOURCES = ["tree_attn.hip", "lmhead.hip", "accept_compact.hip", "layer.hip"]
+HIP_SOURCES = ["tree_attn.hip", "lmhead.hip", "accept_compact.hip", "layer.hip", "linear.hip"]
 HOST_SOURCES = ["host.cpp"]
 ARCH = "gfx950"
 
@@ -63,7 +63,7 @@ def build(verbose: bool = False, extra_flags=()) -> str:
     with ThreadPoolExecutor(min(8, len(jobs))) as ex:
         list(ex.map(lambda c: _run(c, verbose), jobs))
     tmp = LIB + f".tmp{os.getpid()}"
-    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-lhipblaslt", "-o", tmp], verbose)
+    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp], verbose)
     os.replace(tmp, LIB)
     return LIB
 

@@ -11,14 +11,8 @@
 //  * ooo_qk_norm_rope   per-head RMSNorm of q and k, rotation at P + depth,
 //                       q to a [N][Hq][D] buffer, k and v to the cache rows
 //  * ooo_swiglu         silu(gate) * up
-//  * ooo_linear         y = x W^T (+ y), bf16 operands, fp32 accumulation:
-//                       a plain GEMM, run by hipBLASLt
-#include <hipblaslt/hipblaslt.h>
+// The projections between them are ooo_linear (linear.hip).
 #include <math.h>
-
-#include <map>
-#include <mutex>
-#include <tuple>
 
 #include "device_common.h"
 #include "ooo_internal.h"
@@ -140,67 +134,6 @@ __global__ __launch_bounds__(256) void swiglu_kernel(const float* __restrict__ g
   }
 }
 
-// ------------------------------------------------------------ linear layers
-// hipBLASLt in column-major terms: D[O x N] = op(A)[O x K] * B[K x N] (+ C),
-// with A the row-major weight W[O][K] (a K x O column-major matrix,
-// transposed), B the row-major activations X[N][K] (K x N) and D the
-// row-major output Y[N][O] (O x N).  One plan per (device, N, K, O, output
-// type), created on first use.
-struct LtPlan {
-  hipblasLtMatmulDesc_t desc = nullptr;
-  hipblasLtMatrixLayout_t a = nullptr, b = nullptr, c = nullptr;
-  hipblasLtMatmulAlgo_t algo{};
-  size_t ws = 0;
-};
-
-std::mutex g_lt_mu;
-std::map<std::tuple<int, int, int, int, int>, LtPlan> g_lt_plans;
-hipblasLtHandle_t g_lt_handle[64] = {};
-
-int lt_plan(int dev, int N, int K, int O, hipDataType out_t, size_t ws_bytes, LtPlan* plan) {
-  std::lock_guard<std::mutex> lk(g_lt_mu);
-  const auto key = std::make_tuple(dev, N, K, O, (int)out_t);
-  auto it = g_lt_plans.find(key);
-  if (it != g_lt_plans.end() && it->second.ws <= ws_bytes) {
-    *plan = it->second;
-    return OOO_OK;
-  }
-  if (!g_lt_handle[dev])
-    OOO_REQUIRE(hipblasLtCreate(&g_lt_handle[dev]) == HIPBLAS_STATUS_SUCCESS, OOO_ERR_HIP,
-                "ooo_linear: hipblasLtCreate failed");
-  LtPlan p = it != g_lt_plans.end() ? it->second : LtPlan{};
-  if (!p.desc) {
-    const hipblasOperation_t opT = HIPBLAS_OP_T, opN = HIPBLAS_OP_N;
-    bool ok = hipblasLtMatmulDescCreate(&p.desc, HIPBLAS_COMPUTE_32F, HIP_R_32F) == HIPBLAS_STATUS_SUCCESS &&
-              hipblasLtMatmulDescSetAttribute(p.desc, HIPBLASLT_MATMUL_DESC_TRANSA, &opT, sizeof(opT)) ==
-                  HIPBLAS_STATUS_SUCCESS &&
-              hipblasLtMatmulDescSetAttribute(p.desc, HIPBLASLT_MATMUL_DESC_TRANSB, &opN, sizeof(opN)) ==
-                  HIPBLAS_STATUS_SUCCESS &&
-              hipblasLtMatrixLayoutCreate(&p.a, HIP_R_16BF, K, O, K) == HIPBLAS_STATUS_SUCCESS &&
-              hipblasLtMatrixLayoutCreate(&p.b, HIP_R_16BF, K, N, K) == HIPBLAS_STATUS_SUCCESS &&
-              hipblasLtMatrixLayoutCreate(&p.c, out_t, O, N, O) == HIPBLAS_STATUS_SUCCESS;
-    OOO_REQUIRE(ok, OOO_ERR_HIP, "ooo_linear: hipBLASLt descriptor setup failed");
-  }
-  hipblasLtMatmulPreference_t pref;
-  OOO_REQUIRE(hipblasLtMatmulPreferenceCreate(&pref) == HIPBLAS_STATUS_SUCCESS, OOO_ERR_HIP,
-              "ooo_linear: preference setup failed");
-  const uint64_t cap = ws_bytes;
-  hipblasLtMatmulPreferenceSetAttribute(pref, HIPBLASLT_MATMUL_PREF_MAX_WORKSPACE_BYTES, &cap, sizeof(cap));
-  hipblasLtMatmulHeuristicResult_t res[1];
-  int got = 0;
-  const hipblasStatus_t st =
-      hipblasLtMatmulAlgoGetHeuristic(g_lt_handle[dev], p.desc, p.a, p.b, p.c, p.c, pref, 1, res, &got);
-  hipblasLtMatmulPreferenceDestroy(pref);
-  OOO_REQUIRE(st == HIPBLAS_STATUS_SUCCESS && got >= 1, OOO_ERR_UNSUPPORTED,
-              "ooo_linear: no hipBLASLt algorithm for N=%d K=%d O=%d within %zu workspace bytes", N, K, O,
-              ws_bytes);
-  p.algo = res[0].algo;
-  p.ws = res[0].workspaceSize;
-  g_lt_plans[key] = p;
-  *plan = p;
-  return OOO_OK;
-}
-
 }  // namespace
 }  // namespace ooo
 
@@ -267,28 +200,5 @@ extern "C" int ooo_swiglu(const float* gate_up, int32_t n_rows, int32_t intermed
                                                                           (uint16_t*)out);
   const hipError_t e = hipGetLastError();
   OOO_REQUIRE(e == hipSuccess, OOO_ERR_HIP, "ooo_swiglu: launch failed: %s", hipGetErrorString(e));
-  return ooo::ok();
-}
-
-extern "C" size_t ooo_linear_workspace(void) { return (size_t)32 << 20; }
-
-extern "C" int ooo_linear(const void* x, const void* weight, int32_t n_rows, int32_t in_dim, int32_t out_dim,
-                          ooo_dtype out_dt, int32_t accumulate, void* out, void* workspace, size_t ws_bytes,
-                          void* stream) {
-  OOO_REQUIRE(x && weight && out, OOO_ERR_INVALID, "ooo_linear: null pointer");
-  OOO_REQUIRE(n_rows >= 1 && in_dim >= 1 && out_dim >= 1, OOO_ERR_INVALID, "ooo_linear: sizes must be positive");
-  OOO_REQUIRE(out_dt == OOO_F32 || out_dt == OOO_BF16, OOO_ERR_INVALID, "ooo_linear: unknown output dtype %d",
-              (int)out_dt);
-  OOO_REQUIRE(ws_bytes == 0 || workspace, OOO_ERR_INVALID, "ooo_linear: workspace is null");
-  int dev = 0;
-  OOO_REQUIRE(hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64, OOO_ERR_HIP, "ooo_linear: no device");
-  LtPlan p;
-  const int rc = lt_plan(dev, n_rows, in_dim, out_dim, out_dt == OOO_F32 ? HIP_R_32F : HIP_R_16BF, ws_bytes, &p);
-  if (rc != OOO_OK) return rc;
-  const float alpha = 1.f, beta = accumulate ? 1.f : 0.f;
-  const hipblasStatus_t st = hipblasLtMatmul(g_lt_handle[dev], p.desc, &alpha, weight, p.a, x, p.b, &beta, out, p.c,
-                                             out, p.c, &p.algo, workspace, ws_bytes,
-                                             reinterpret_cast<hipStream_t>(stream));
-  OOO_REQUIRE(st == HIPBLAS_STATUS_SUCCESS, OOO_ERR_HIP, "ooo_linear: hipblasLtMatmul failed (%d)", (int)st);
   return ooo::ok();
 }

@@ -1,0 +1,336 @@
+// Projections of the target decoder around the verification path: the
+// q/k/v, output and MLP projections of every layer (Section 4.5: the target
+// scores the tree in one forward pass; Section 5: Qwen3 targets).  With the
+// trie's N <= 256 rows these are skinny GEMMs, Y[N][O] = X[N][K] W[O][K]^T,
+// bound by streaming W from HBM once.
+//
+// Design (the LM head's streaming scheme, made shape-independent):
+//  * W is packed once into 16 KiB blocks of 128 rows x 64 columns (the LM
+//    head's layout, ooo_linear_pack); the work is the sequence of (128-row
+//    tile, 64-column chunk) blocks in tile-major order.
+//  * Stream-K: a persistent grid (one block per CU) where block b takes the
+//    contiguous run of chunks [C b / B, C (b + 1) / B).  Every block streams
+//    the same number of bytes whatever O and K are; a run covers the end of
+//    one tile and the start of the next.
+//  * Inside a block: two loader waves DMA the W chunk (two 32-row slots
+//    each) and a third the X chunk into a 6-stage LDS ring; four compute
+//    waves run mfma_f32_32x32x16_bf16 (32 W rows x the nodes each).
+//  * At the end of each tile segment a block stores its partial sums (fp32,
+//    [node][128 rows]) in the workspace; a reduce kernel adds a tile's
+//    partials in block order (deterministic, no atomics) and applies the
+//    epilogue: store fp32 or bf16, add into an fp32 output (the residual
+//    rows), or silu(gate) * up of a fused gate/up projection.
+#include <math.h>
+
+#include "device_common.h"
+#include "ooo_internal.h"
+
+namespace ooo {
+namespace {
+
+#define OOO_LDS(p) ((__attribute__((address_space(3))) void*)(p))
+#define OOO_GLB(p) ((const __attribute__((address_space(1))) void*)(p))
+
+__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x0F70);
+}
+
+constexpr int kRows = 128;  // W rows per tile (4 compute waves x 32)
+
+template <int NB>
+struct Ring {
+  static constexpr int XR = 32 * NB;        // node rows staged (padded)
+  static constexpr int WS = kRows * 128;    // bytes of a W chunk
+  static constexpr int XS = XR * 128;       // bytes of an X chunk
+  static constexpr int NS = NB == 1 ? 7 : NB == 2 ? 6 : NB == 4 ? 4 : 3;
+  static constexpr int XREG = NS * WS;
+  static constexpr int BYTES = NS * (WS + XS);
+  static constexpr int WDMA = WS / 1024 / 2;  // DMA instructions per W chunk and W loader
+  static constexpr int XDMA = XS / 1024;
+  static_assert((NS - 2) * WDMA <= 63 && (NS - 2) * XDMA <= 63, "vmcnt range");
+  static_assert(BYTES <= 160 * 1024, "LDS capacity");
+};
+
+template <int PER, int MAXA>
+__device__ __forceinline__ void wait_chunks(int ahead) {
+  static_assert(MAXA <= 5, "ring depth");
+  if (MAXA >= 5 && ahead >= 5) wait_vmcnt<(MAXA >= 5 ? 5 * PER : 0)>();
+  else if (MAXA >= 4 && ahead == 4) wait_vmcnt<(MAXA >= 4 ? 4 * PER : 0)>();
+  else if (MAXA >= 3 && ahead == 3) wait_vmcnt<(MAXA >= 3 ? 3 * PER : 0)>();
+  else if (MAXA >= 2 && ahead == 2) wait_vmcnt<(MAXA >= 2 ? 2 * PER : 0)>();
+  else if (ahead == 1) wait_vmcnt<PER>();
+  else wait_vmcnt<0>();
+}
+
+// first chunk of block b's run
+__host__ __device__ __forceinline__ long long run_lo(long long C, int b, int B) { return C * b / B; }
+
+template <int NB, bool PACKED>
+__global__ __launch_bounds__(448) void linear_bf16_kernel(const uint16_t* __restrict__ X,
+                                                          const uint16_t* __restrict__ Wt, int N, int K, int O,
+                                                          int seg_per_block, float* __restrict__ part) {
+  using R = Ring<NB>;
+  constexpr int NPAD = 32 * NB;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[R::BYTES];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int KC = K / 64;
+  const int tiles = (O + kRows - 1) / kRows;
+  const long long C = (long long)tiles * KC;
+  const int b = (int)blockIdx.x, B = (int)gridDim.x;
+  const long long lo = run_lo(C, b, B);
+  const int total = (int)(run_lo(C, b + 1, B) - lo);  // chunks of this block (>= 1: B <= C)
+  const int first_tile = (int)(lo / KC);
+
+  if (wave >= 4) {
+    // ------------------------------------------ loaders: W rows 0-63 (4), 64-127 (5), X (6)
+    const bool is_x = wave == 6;
+    const int half = wave - 4;
+    // (tile, chunk) of the next chunk to issue; issues come in order
+    int it = first_tile, ikc = (int)(lo - (long long)first_tile * KC);
+    auto issue = [&](int q, int stage) {
+      const int t = it, kc = ikc;
+      if (++ikc == KC) {
+        ikc = 0;
+        ++it;
+      }
+      if (!is_x) {
+        uint8_t* dst = lds + stage * R::WS + half * (R::WS / 2);
+        if (PACKED) {
+          const uint16_t* src = Wt + ((size_t)t * KC + kc) * (kRows * 64) + half * (kRows * 32) + lane * 8;
+#pragma unroll
+          for (int j = 0; j < R::WDMA; ++j)
+            __builtin_amdgcn_global_load_lds(OOO_GLB(src + j * 512), OOO_LDS(dst + j * 1024), 16, 0, 0);
+        } else {
+#pragma unroll
+          for (int j = 0; j < R::WDMA; ++j) {
+            const int r = half * 64 + 8 * j + lane / 8;  // tile row; lane = (row, physical piece)
+            const int pc = (lane % 8) ^ (r % 8);
+            const int row = min(t * kRows + r, O - 1);
+            __builtin_amdgcn_global_load_lds(OOO_GLB(Wt + (size_t)row * K + kc * 64 + pc * 8),
+                                             OOO_LDS(dst + j * 1024), 16, 0, 0);
+          }
+        }
+      } else {
+        uint8_t* dst = lds + R::XREG + stage * R::XS;
+#pragma unroll
+        for (int j = 0; j < R::XDMA; ++j) {
+          const int r = 8 * j + lane / 8;
+          const int pc = (lane % 8) ^ (r % 8);
+          const int row = min(r, N - 1);
+          __builtin_amdgcn_global_load_lds(OOO_GLB(X + (size_t)row * K + kc * 64 + pc * 8),
+                                           OOO_LDS(dst + j * 1024), 16, 0, 0);
+        }
+      }
+    };
+    for (int q = 0; q < R::NS - 1 && q < total; ++q) issue(q, q);
+    for (int q = 0; q < total; ++q) {
+      const int ahead = min(R::NS - 2, total - 1 - q);
+      if (is_x) wait_chunks<R::XDMA, R::NS - 2>(ahead);
+      else wait_chunks<R::WDMA, R::NS - 2>(ahead);
+      wg_barrier();
+      if (q + R::NS - 1 < total) issue(q + R::NS - 1, (q + R::NS - 1) % R::NS);
+    }
+    return;
+  }
+
+  // ------------------------------------------------------------------ compute
+  const int c = lane & 31, u = lane >> 5;
+  uint32_t off[4];  // piece 2s+u of row c, swizzled
+#pragma unroll
+  for (int s4 = 0; s4 < 4; ++s4) off[s4] = c * 128 + (((2 * s4 + u) ^ (c % 8)) << 4);
+  const uint32_t wrow = wave * 32 * 128;
+  f32x16 acc[NB];
+  int t = first_tile, kc = (int)(lo - (long long)first_tile * KC) - 1;
+  for (int q = 0; q < total; ++q) {
+    if (++kc == KC) {
+      kc = 0;
+      ++t;
+    }
+    if (q == 0 || kc == 0) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x16{};
+    }
+    const int stage = q % R::NS;
+    wg_barrier();
+    const uint8_t* Ws = lds + stage * R::WS + wrow;
+    const uint8_t* Xs = lds + R::XREG + stage * R::XS;
+    bf16x8 af[4], bf[NB][4];
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4) {
+      af[s4] = as_bf16x8(*reinterpret_cast<const u32x4*>(Ws + off[s4]));
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) bf[nb][s4] = as_bf16x8(*reinterpret_cast<const u32x4*>(Xs + nb * 4096 + off[s4]));
+    }
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) acc[nb] = mfma32(af[s4], bf[nb][s4], acc[nb]);
+    if (q == total - 1 || kc == KC - 1) {
+      // segment done: acc[nb][j] = partial of tile row wave*32 + 8(j/4) + 4u + j%4, node 32nb + c
+      float* dst = part + ((size_t)b * seg_per_block + (t - first_tile)) * NPAD * kRows;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int jq = 0; jq < 4; ++jq)
+          *reinterpret_cast<f32x4*>(dst + (size_t)(32 * nb + c) * kRows + wave * 32 + 8 * jq + 4 * u) =
+              f32x4{acc[nb][4 * jq], acc[nb][4 * jq + 1], acc[nb][4 * jq + 2], acc[nb][4 * jq + 3]};
+    }
+  }
+}
+
+enum Epi { kStoreF32 = 0, kStoreBF16 = 1, kAddF32 = 2, kSwiGLU = 3 };
+
+// Workspace slots holding tile t's partials, in block order (the blocks
+// whose runs intersect the tile's chunks [t KC, (t + 1) KC)); returns the
+// count.  Called by one thread per reduce block.
+__device__ int tile_slots(long long C, int B, int KC, int seg, int t, int* slots) {
+  const long long g0 = (long long)t * KC, g1 = g0 + KC;
+  int b = (int)(g0 * B / C);
+  while (b + 1 < B && run_lo(C, b + 1, B) <= g0) ++b;
+  while (b > 0 && run_lo(C, b, B) > g0) --b;
+  int n = 0;
+  for (; b < B && run_lo(C, b, B) < g1; ++b) slots[n++] = b * seg + (t - (int)(run_lo(C, b, B) / KC));
+  return n;
+}
+
+// Four blocks per output tile (per gate tile for kSwiGLU), 32 rows each;
+// thread item (n, 4 consecutive rows), so partial reads are 16 bytes and
+// contiguous across threads.  Partials are added in block order; the slot
+// loop is unrolled so that its loads are in flight together.
+__device__ __forceinline__ f32x4 slot_sum(const float* __restrict__ part, const int* slots, int ns, size_t stride,
+                                          size_t e) {
+  f32x4 s = {0.f, 0.f, 0.f, 0.f};
+  int i = 0;
+  for (; i + 4 <= ns; i += 4) {
+    const f32x4 a = *reinterpret_cast<const f32x4*>(part + slots[i] * stride + e);
+    const f32x4 b = *reinterpret_cast<const f32x4*>(part + slots[i + 1] * stride + e);
+    const f32x4 c = *reinterpret_cast<const f32x4*>(part + slots[i + 2] * stride + e);
+    const f32x4 d = *reinterpret_cast<const f32x4*>(part + slots[i + 3] * stride + e);
+    s += a;
+    s += b;
+    s += c;
+    s += d;
+  }
+  for (; i < ns; ++i) s += *reinterpret_cast<const f32x4*>(part + slots[i] * stride + e);
+  return s;
+}
+
+__global__ __launch_bounds__(256) void linear_reduce_kernel(const float* __restrict__ part, int N, int npad, int K,
+                                                            int O, int B, int seg, int epi, void* __restrict__ out,
+                                                            int inter) {
+  __shared__ int slots[2][256];
+  __shared__ int nslots[2];
+  const int t = blockIdx.x >> 2, quarter = blockIdx.x & 3;
+  const int KC = K / 64;
+  const int tiles = (O + kRows - 1) / kRows;
+  const long long C = (long long)tiles * KC;
+  if (threadIdx.x < 2 && (threadIdx.x == 0 || epi == kSwiGLU))
+    nslots[threadIdx.x] = tile_slots(C, B, KC, seg, threadIdx.x ? t + inter / kRows : t, slots[threadIdx.x]);
+  __syncthreads();
+  const size_t stride = (size_t)npad * kRows;  // floats per slot
+  const int ns0 = nslots[0], ns1 = epi == kSwiGLU ? nslots[1] : 0;
+  for (int item = threadIdx.x; item < N * 8; item += 256) {
+    const int n = item >> 3, r = quarter * 32 + 4 * (item & 7);
+    const size_t e = (size_t)n * kRows + r;
+    const int col = t * kRows + r;
+    const f32x4 sv = slot_sum(part, slots[0], ns0, stride, e);
+    if (epi == kSwiGLU) {
+      const f32x4 uv = slot_sum(part, slots[1], ns1, stride, e);
+      uint16_t* o = reinterpret_cast<uint16_t*>(out) + (size_t)n * inter + col;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (col + j < inter) o[j] = (uint16_t)(pack_bf16x2(sv[j] / (1.f + expf(-sv[j])) * uv[j], 0.f) & 0xFFFFu);
+      continue;
+    }
+    const size_t o = (size_t)n * O + col;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (col + j >= O) break;
+      if (epi == kStoreF32) reinterpret_cast<float*>(out)[o + j] = sv[j];
+      else if (epi == kAddF32) reinterpret_cast<float*>(out)[o + j] += sv[j];
+      else reinterpret_cast<uint16_t*>(out)[o + j] = (uint16_t)(pack_bf16x2(sv[j], 0.f) & 0xFFFFu);
+    }
+  }
+}
+
+struct LinPlan {
+  int nb, blocks, seg;
+  size_t ws_bytes;
+};
+
+LinPlan lin_plan(int N, int K, int O) {
+  LinPlan p{};
+  p.nb = N <= 32 ? 1 : N <= 64 ? 2 : N <= 128 ? 4 : 8;
+  const long long C = (long long)((O + kRows - 1) / kRows) * (K / 64);
+  const int cus = device_cus() < 256 ? device_cus() : 256;  // the reduce kernel keeps <= 256 slots per tile
+  p.blocks = (int)(C < cus ? C : cus);
+  const long long run = (C + p.blocks - 1) / p.blocks;
+  p.seg = (int)(run / (K / 64)) + 2;  // tiles a run can touch
+  p.ws_bytes = (size_t)p.blocks * p.seg * (32 * p.nb) * kRows * sizeof(float);
+  return p;
+}
+
+}  // namespace
+}  // namespace ooo
+
+using namespace ooo;
+
+extern "C" size_t ooo_linear_packed_bytes(int32_t out_dim, int32_t in_dim) {
+  return ooo_lmhead_packed_bytes(out_dim, in_dim, OOO_BF16);
+}
+
+extern "C" int ooo_linear_pack(const void* weight, int32_t out_dim, int32_t in_dim, void* packed, size_t packed_bytes,
+                               void* stream) {
+  return ooo_lmhead_pack(weight, out_dim, in_dim, OOO_BF16, packed, packed_bytes, stream);
+}
+
+extern "C" size_t ooo_linear_workspace(int32_t n_rows, int32_t in_dim, int32_t out_dim) {
+  if (n_rows < 1 || n_rows > 256 || in_dim < 64 || in_dim % 64 || out_dim < 1) return 0;
+  return lin_plan(n_rows, in_dim, out_dim).ws_bytes;
+}
+
+extern "C" int ooo_linear(const void* x, const void* weight, int32_t n_rows, int32_t in_dim, int32_t out_dim,
+                          int32_t weight_layout, ooo_epilogue epilogue, void* out, void* workspace, size_t ws_bytes,
+                          void* stream) {
+  OOO_REQUIRE(x && weight && out, OOO_ERR_INVALID, "ooo_linear: null pointer");
+  OOO_REQUIRE(n_rows >= 1 && in_dim >= 1 && out_dim >= 1, OOO_ERR_INVALID, "ooo_linear: sizes must be positive");
+  OOO_REQUIRE(weight_layout == OOO_W_ROWS || weight_layout == OOO_W_PACKED, OOO_ERR_INVALID,
+              "ooo_linear: unknown weight layout %d", weight_layout);
+  OOO_REQUIRE(epilogue >= OOO_EPI_STORE_F32 && epilogue <= OOO_EPI_SWIGLU_BF16, OOO_ERR_INVALID,
+              "ooo_linear: unknown epilogue %d", (int)epilogue);
+  OOO_REQUIRE(in_dim % 64 == 0, OOO_ERR_UNSUPPORTED, "ooo_linear: in_dim %% 64 != 0");
+  OOO_REQUIRE(n_rows <= 256, OOO_ERR_UNSUPPORTED, "ooo_linear: at most 256 rows");
+  OOO_REQUIRE(epilogue != OOO_EPI_SWIGLU_BF16 || out_dim % 256 == 0, OOO_ERR_UNSUPPORTED,
+              "ooo_linear: the SwiGLU epilogue needs out_dim %% 256 == 0 (gate and up halves of whole tiles)");
+  const LinPlan p = lin_plan(n_rows, in_dim, out_dim);
+  OOO_REQUIRE(workspace && ws_bytes >= p.ws_bytes, OOO_ERR_CAPACITY,
+              "ooo_linear: workspace of %zu bytes needed (got %zu)", p.ws_bytes, ws_bytes);
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const uint16_t* X = (const uint16_t*)x;
+  const uint16_t* W = (const uint16_t*)weight;
+  float* part = (float*)workspace;
+  const bool pk = weight_layout == OOO_W_PACKED;
+#define OOO_LIN_LAUNCH(NBV)                                                                                        \
+  do {                                                                                                            \
+    if (pk)                                                                                                       \
+      linear_bf16_kernel<NBV, true><<<p.blocks, 448, 0, st>>>(X, W, n_rows, in_dim, out_dim, p.seg, part);         \
+    else                                                                                                          \
+      linear_bf16_kernel<NBV, false><<<p.blocks, 448, 0, st>>>(X, W, n_rows, in_dim, out_dim, p.seg, part);        \
+  } while (0)
+  if (p.nb == 1) OOO_LIN_LAUNCH(1);
+  else if (p.nb == 2) OOO_LIN_LAUNCH(2);
+  else if (p.nb == 4) OOO_LIN_LAUNCH(4);
+  else OOO_LIN_LAUNCH(8);
+#undef OOO_LIN_LAUNCH
+  const int tiles = (out_dim + kRows - 1) / kRows;
+  const int rgrid = 4 * (epilogue == OOO_EPI_SWIGLU_BF16 ? tiles / 2 : tiles);
+  linear_reduce_kernel<<<rgrid, 256, 0, st>>>(part, n_rows, 32 * p.nb, in_dim, out_dim, p.blocks, p.seg, (int)epilogue,
+                                              out, out_dim / 2);
+  const hipError_t e = hipGetLastError();
+  OOO_REQUIRE(e == hipSuccess, OOO_ERR_HIP, "ooo_linear: launch failed: %s", hipGetErrorString(e));
+  return ooo::ok();
+}

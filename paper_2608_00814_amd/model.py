@@ -8,17 +8,18 @@ compaction):
     h = embedding[token]                                  ooo_embed_rows
     per layer:
         x   = rmsnorm(h)                                  ooo_rmsnorm
-        qkv = x Wqkv^T                                    ooo_linear
+        qkv = x Wqkv^T                                    ooo_linear (bf16 out)
         q, cache[P + i] <- k, v  (norms, rotation at P + depth)   ooo_qk_norm_rope
         o   = tree attention                              ooo_tree_attn
-        h  += o Wo^T                                      ooo_linear (accumulate)
+        h  += o Wo^T                                      ooo_linear (add into h)
         x   = rmsnorm(h)                                  ooo_rmsnorm
-        a   = silu(x Wg^T) * (x Wu^T)                     ooo_linear + ooo_swiglu
-        h  += a Wd^T                                      ooo_linear (accumulate)
+        a   = silu(x Wg^T) * (x Wu^T)                     ooo_linear (SwiGLU epilogue)
+        h  += a Wd^T                                      ooo_linear (add into h)
     X = rmsnorm(h); greedy tokens; accept; compact        (VerifyRunner)
 
 The residual rows stay in float32; every projection reads bf16 operands and
-accumulates in float32.
+accumulates in float32.  Projection weights are packed once, at load, into
+the streaming layout of ooo_linear_pack.
 """
 
 from __future__ import annotations
@@ -49,28 +50,32 @@ class ModelRunner:
         self.vr.set_weight(_bits_to_dev(lm_head, dev))
         self.emb = _bits_to_dev(embedding, dev)
         self.final_norm = _bits_to_dev(final_norm, dev)
-        self.layers: List[Dict[str, torch.Tensor]] = []
+        self.layers: List[Dict[str, object]] = []
+        pk = lambda a: ooo.linear_pack(_bits_to_dev(a, dev))
         for lw in layers:
             self.layers.append({
                 "in_norm": _bits_to_dev(lw["in_norm"], dev),
-                "w_qkv": _bits_to_dev(lw["w_qkv"], dev),
+                "w_qkv": pk(lw["w_qkv"]),
                 "q_norm": _bits_to_dev(lw["q_norm"], dev),
                 "k_norm": _bits_to_dev(lw["k_norm"], dev),
-                "w_o": _bits_to_dev(lw["w_o"], dev),
+                "w_o": pk(lw["w_o"]),
                 "post_norm": _bits_to_dev(lw["post_norm"], dev),
-                # gate rows, then up rows: one projection feeds ooo_swiglu
-                "w_gu": _bits_to_dev(np.concatenate([lw["w_gate"], lw["w_up"]], axis=0), dev),
-                "w_down": _bits_to_dev(lw["w_down"], dev),
+                # gate rows, then up rows: the SwiGLU epilogue pairs them
+                "w_gu": pk(np.concatenate([lw["w_gate"], lw["w_up"]], axis=0)),
+                "w_down": pk(lw["w_down"]),
             })
+            torch.cuda.synchronize(dev)  # the row-major copies can go
         n, H = cfg.max_nodes, cfg.hidden
         self.h = torch.zeros(n, H, dtype=torch.float32, device=dev)
         self.x = torch.zeros(n, H, dtype=torch.bfloat16, device=dev)
         self.xf = torch.zeros(n, H, dtype=torch.bfloat16, device=dev)  # LM-head input
         self.qkv = torch.zeros(n, cfg.qkv_rows, dtype=torch.bfloat16, device=dev)
         self.q = torch.zeros(n, cfg.n_q_heads, cfg.head_dim, dtype=torch.bfloat16, device=dev)
-        self.gu = torch.zeros(n, 2 * cfg.intermediate, dtype=torch.float32, device=dev)
         self.act = torch.zeros(n, cfg.intermediate, dtype=torch.bfloat16, device=dev)
-        self.lin_ws = torch.empty(ooo.linear_workspace(), dtype=torch.uint8, device=dev)
+        H, I, A = cfg.hidden, cfg.intermediate, cfg.n_q_heads * cfg.head_dim
+        need = max(ooo.linear_workspace(nn, k, o) for nn in range(1, n + 1)
+                   for k, o in ((H, cfg.qkv_rows), (A, H), (H, 2 * I), (I, H)))
+        self.lin_ws = torch.empty(need, dtype=torch.uint8, device=dev)
 
     # -- host ---------------------------------------------------------------
     def pack(self, root_token: int, cand_tokens: np.ndarray, cand_offsets: np.ndarray, keep: bool = True):
@@ -88,16 +93,15 @@ class ModelRunner:
         ooo.embed_rows(self.emb, vr.token, N, self.h)
         for l, w in enumerate(self.layers):
             ooo.rmsnorm(self.h, w["in_norm"], cfg.eps, self.x, n_rows=N)
-            ooo.linear(self.x, w["w_qkv"], self.qkv, n_rows=N, workspace=ws)
+            ooo.linear(self.x, w["w_qkv"], self.qkv, ooo.EPI_STORE_BF16, ws, n_rows=N)
             ooo.qk_norm_rope(self.qkv, w["q_norm"], w["k_norm"], cfg.eps, vr.depth, N, P, cfg.rope_theta,
                              cfg.n_q_heads, cfg.n_kv_heads, self.q, k_cache[l], v_cache[l])
             vr.attention(l, self.q, k_cache[l], v_cache[l], P)
             o = vr.out[l].view(cfg.max_nodes, cfg.n_q_heads * cfg.head_dim)
-            ooo.linear(o, w["w_o"], self.h, n_rows=N, accumulate=True, workspace=ws)
+            ooo.linear(o, w["w_o"], self.h, ooo.EPI_ADD_F32, ws, n_rows=N)
             ooo.rmsnorm(self.h, w["post_norm"], cfg.eps, self.x, n_rows=N)
-            ooo.linear(self.x, w["w_gu"], self.gu, n_rows=N, workspace=ws)
-            ooo.swiglu(self.gu, self.act, n_rows=N)
-            ooo.linear(self.act, w["w_down"], self.h, n_rows=N, accumulate=True, workspace=ws)
+            ooo.linear(self.x, w["w_gu"], self.act, ooo.EPI_SWIGLU_BF16, ws, n_rows=N)
+            ooo.linear(self.act, w["w_down"], self.h, ooo.EPI_ADD_F32, ws, n_rows=N)
         ooo.rmsnorm(self.h, self.final_norm, cfg.eps, self.xf, n_rows=N)
 
     def device_step(self, k_cache: torch.Tensor, v_cache: torch.Tensor, prefix_len: int,

@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libooo.so")
 OK, ERR_INVALID, ERR_UNSUPPORTED, ERR_CAPACITY, ERR_HIP = 0, -1, -2, -3, -4
 F32, BF16 = 0, 1
 W_ROWS, W_PACKED = 0, 1  # ooo_weight_layout
+EPI_STORE_F32, EPI_STORE_BF16, EPI_ADD_F32, EPI_SWIGLU_BF16 = 0, 1, 2, 3  # ooo_epilogue
 
 _c_i32p = ctypes.POINTER(ctypes.c_int32)
 _c_u64p = ctypes.POINTER(ctypes.c_uint64)
@@ -49,8 +50,10 @@ SIGNATURES = {
                                       _i32, _vp]),
     "ooo_embed_rows": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _vp, _vp]),
     "ooo_rmsnorm": (ctypes.c_int, [_vp, _vp, _i32, _i32, ctypes.c_float, _vp, _vp]),
-    "ooo_linear_workspace": (_sz, []),
-    "ooo_linear": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, ctypes.c_int, _i32, _vp, _vp, _sz, _vp]),
+    "ooo_linear_workspace": (_sz, [_i32, _i32, _i32]),
+    "ooo_linear_packed_bytes": (_sz, [_i32, _i32]),
+    "ooo_linear_pack": (ctypes.c_int, [_vp, _i32, _i32, _vp, _sz, _vp]),
+    "ooo_linear": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, ctypes.c_int, _vp, _vp, _sz, _vp]),
     "ooo_qk_norm_rope": (ctypes.c_int, [_vp, _vp, _vp, ctypes.c_float, _vp, _i32, _i32, ctypes.c_double, _i32,
                                         _i32, _i32, _vp, _vp, _vp, _i64, _vp]),
     "ooo_swiglu": (ctypes.c_int, [_vp, _i32, _i32, _vp, _vp]),
@@ -347,21 +350,46 @@ def rmsnorm(h, weight, eps: float, out, n_rows: Optional[int] = None, stream=Non
                              _stream(stream)))
 
 
-def linear_workspace() -> int:
-    return int(lib().ooo_linear_workspace())
+def linear_workspace(n_rows: int, in_dim: int, out_dim: int) -> int:
+    return int(lib().ooo_linear_workspace(n_rows, in_dim, out_dim))
 
 
-def linear(x, weight, out, n_rows: Optional[int] = None, accumulate: bool = False, workspace=None,
-           stream=None) -> None:
-    """out[:n] (+)= x[:n] @ weight.T with x bf16 [rows][in], weight bf16
-    [out][in], out float32 or bf16 [rows][out]."""
-    for t, nm in ((x, "x"), (weight, "weight"), (out, "out")):
-        _dev(t, nm)
-    n = x.shape[0] if n_rows is None else n_rows
+class PackedLinear:
+    """A projection weight in the streaming layout of ooo_linear_pack: a flat
+    uint8 device tensor plus the logical [out_dim][in_dim] shape."""
+
+    def __init__(self, data, out_dim: int, in_dim: int):
+        self.data, self.out_dim, self.in_dim = data, out_dim, in_dim
+        self.shape = (out_dim, in_dim)
+
+
+def linear_pack(weight, stream=None) -> PackedLinear:
+    """Packs a [out][in] bf16 device weight (allocates the packed copy)."""
+    import torch
+    _dev(weight, "weight")
     O, K = weight.shape
-    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    _check(lib().ooo_linear(x.data_ptr(), weight.data_ptr(), n, K, O, dtype_code(out), int(bool(accumulate)),
-                            out.data_ptr(), _ptr(workspace), ws_bytes, _stream(stream)))
+    need = int(lib().ooo_linear_packed_bytes(O, K))
+    if need == 0:
+        raise OooError(ERR_UNSUPPORTED, f"ooo_linear_pack: cannot pack a [{O}][{K}] weight")
+    data = torch.empty(need, dtype=torch.uint8, device=weight.device)
+    _check(lib().ooo_linear_pack(weight.data_ptr(), O, K, data.data_ptr(), need, _stream(stream)))
+    return PackedLinear(data, O, K)
+
+
+def linear(x, weight, out, epilogue: int, workspace, n_rows: Optional[int] = None, stream=None) -> None:
+    """out (epilogue)= x[:n] @ weight.T: x bf16 [rows][in]; weight bf16
+    [out][in] or a PackedLinear; out float32 or bf16 per the epilogue."""
+    _dev(x, "x")
+    _dev(out, "out")
+    n = x.shape[0] if n_rows is None else n_rows
+    if isinstance(weight, PackedLinear):
+        wptr, layout, (O, K) = weight.data.data_ptr(), W_PACKED, weight.shape
+    else:
+        _dev(weight, "weight")
+        wptr, layout, (O, K) = weight.data_ptr(), W_ROWS, weight.shape
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib().ooo_linear(x.data_ptr(), wptr, n, K, O, layout, int(epilogue), out.data_ptr(), workspace.data_ptr(),
+                            ws_bytes, _stream(stream)))
 
 
 def qk_norm_rope(qkv, q_norm, k_norm, eps: float, depth, n_nodes: int, prefix_len: int, rope_theta: float,

@@ -27,7 +27,7 @@ def declared_functions():
 
 def test_exports_match_header():
     names = declared_functions()
-    assert len(names) == 18
+    assert len(names) == 20
     assert set(names) == set(ooo.SIGNATURES)
     lib = ooo.lib()
     for n in names:
@@ -151,10 +151,19 @@ def test_layer_entry_points_validate_on_host():
     assert L.ooo_embed_rows(fake, fake, 0, 64, 100, fake, None) == ooo.ERR_INVALID
     assert L.ooo_rmsnorm(fake, None, 4, 64, 1e-6, fake, None) == ooo.ERR_INVALID
     assert L.ooo_rmsnorm(fake, fake, 4, 64, -1.0, fake, None) == ooo.ERR_INVALID
-    assert L.ooo_linear(fake, fake, 0, 64, 64, ooo.BF16, 0, fake, None, 0, None) == ooo.ERR_INVALID
-    assert L.ooo_linear(None, fake, 4, 64, 64, ooo.BF16, 0, fake, None, 0, None) == ooo.ERR_INVALID
-    assert L.ooo_linear(fake, fake, 4, 64, 64, 7, 0, fake, None, 0, None) == ooo.ERR_INVALID
-    assert L.ooo_linear(fake, fake, 4, 64, 64, ooo.F32, 0, fake, None, 1024, None) == ooo.ERR_INVALID
+    lin = lambda n=4, k=64, o=64, lay=ooo.W_PACKED, epi=ooo.EPI_STORE_F32, x=fake, ws=fake, wsb=1 << 30: \
+        L.ooo_linear(x, fake, n, k, o, lay, epi, fake, ws, wsb, None)
+    assert lin(n=0) == ooo.ERR_INVALID
+    assert lin(x=None) == ooo.ERR_INVALID
+    assert lin(lay=7) == ooo.ERR_INVALID
+    assert lin(epi=9) == ooo.ERR_INVALID
+    assert lin(k=96) == ooo.ERR_UNSUPPORTED
+    assert lin(n=300) == ooo.ERR_UNSUPPORTED
+    assert lin(o=384, epi=ooo.EPI_SWIGLU_BF16) == ooo.ERR_UNSUPPORTED
+    assert lin(wsb=16) == ooo.ERR_CAPACITY
+    assert lin(ws=None) == ooo.ERR_CAPACITY
+    assert ooo.linear_workspace(64, 4096, 6144) > 0 and ooo.linear_workspace(64, 100, 64) == 0
+    assert ooo.lib().ooo_linear_packed_bytes(300, 128) == 384 * 128 * 2
     args = dict(qkv=fake, qn=fake, kn=fake, eps=1e-6, depth=fake, N=4, P=10, theta=1e6, Hq=4, Hkv=2, D=128,
                 q=fake, kc=fake, vc=fake, cap=100)
 
@@ -170,7 +179,6 @@ def test_layer_entry_points_validate_on_host():
     assert qk(D=96) == ooo.ERR_UNSUPPORTED
     assert L.ooo_swiglu(None, 4, 64, fake, None) == ooo.ERR_INVALID
     assert L.ooo_swiglu(fake, 4, 0, fake, None) == ooo.ERR_INVALID
-    assert ooo.linear_workspace() > 0
 
 
 def test_device_entry_points_validate_on_host():

@@ -56,24 +56,36 @@ def test_rmsnorm(N, H):
 
 
 @pytest.mark.parametrize("N,K,O", [(64, 4096, 6144), (64, 4096, 4096), (37, 4096, 24576), (64, 12288, 4096),
-                                   (1, 256, 1152), (5, 512, 256)])
-def test_linear(N, K, O):
-    print(f"case linear N={N} K={K} O={O}", flush=True)
+                                   (1, 256, 1152), (5, 512, 256), (200, 1024, 3000), (33, 64, 130)])
+@pytest.mark.parametrize("packed", [True, False], ids=["packed", "rows"])
+def test_linear(N, K, O, packed):
+    """Every epilogue of the streaming projection, both weight layouts, and
+    bitwise-repeatable results."""
+    print(f"case linear N={N} K={K} O={O} packed={packed}", flush=True)
     rs = np.random.default_rng(N + K + O)
     x, w = _bits(rs, (N, K)), _bits(rs, (O, K), 0.02)
     xd, wd = _dev_bf16(x), _dev_bf16(w)
+    wl_ = ooo.linear_pack(wd) if packed else wd
     ref = f64(x) @ f64(w).T
-    ws = torch.empty(ooo.linear_workspace(), dtype=torch.uint8, device=DEV)
-    y32 = torch.empty(N, O, dtype=torch.float32, device=DEV)
-    ooo.linear(xd, wd, y32, workspace=ws)
+    ws = torch.empty(ooo.linear_workspace(N, K, O), dtype=torch.uint8, device=DEV)
+    y32 = torch.full((N, O), float("nan"), dtype=torch.float32, device=DEV)
+    ooo.linear(xd, wl_, y32, ooo.EPI_STORE_F32, ws)
     assert gh.row_rel_err(y32.double().cpu().numpy(), ref) <= 1e-4
+    again = torch.empty_like(y32)
+    ooo.linear(xd, wl_, again, ooo.EPI_STORE_F32, ws)
+    assert torch.equal(y32, again)
     y16 = torch.empty(N, O, dtype=torch.bfloat16, device=DEV)
-    ooo.linear(xd, wd, y16, workspace=ws)
+    ooo.linear(xd, wl_, y16, ooo.EPI_STORE_BF16, ws)
     assert gh.row_rel_err(_host_f64(y16), ref) <= TOL
     base = rs.normal(size=(N, O)).astype(np.float32)
     acc = torch.from_numpy(base).to(DEV)
-    ooo.linear(xd, wd, acc, accumulate=True, workspace=ws)
+    ooo.linear(xd, wl_, acc, ooo.EPI_ADD_F32, ws)
     assert gh.row_rel_err(acc.double().cpu().numpy(), ref + base) <= 1e-4
+    if O % 256 == 0:
+        I = O // 2
+        act = torch.empty(N, I, dtype=torch.bfloat16, device=DEV)
+        ooo.linear(xd, wl_, act, ooo.EPI_SWIGLU_BF16, ws)
+        assert gh.row_rel_err(_host_f64(act), om.silu(ref[:, :I]) * ref[:, I:]) <= TOL
     torch.cuda.synchronize()
 
 
