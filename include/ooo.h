@@ -284,7 +284,8 @@ int ooo_kv_compact(void* k_cache, void* v_cache, int32_t n_layers, int32_t n_kv_
  *   tokens   [n_nodes] int32 (the packed trie's tokens)
  *   h        [n_nodes][hidden_dim] float32 output
  * A token outside [0, vocab) gives a row of NaN.
- * Errors: OOO_ERR_INVALID (null pointers, sizes < 1), OOO_ERR_HIP.
+ * Errors: OOO_ERR_INVALID (null pointers, sizes < 1), OOO_ERR_UNSUPPORTED
+ * (hidden_dim % 8 != 0), OOO_ERR_HIP.
  */
 int ooo_embed_rows(const void* table, const int32_t* tokens, int32_t n_nodes, int32_t hidden_dim,
                    int32_t vocab, float* h, void* stream);
@@ -297,7 +298,8 @@ int ooo_embed_rows(const void* table, const int32_t* tokens, int32_t n_nodes, in
  *   h        [n_rows][dim] float32 residual rows
  *   weight   [dim] bf16
  *   out      [n_rows][dim] bf16; must not alias h
- * Errors: OOO_ERR_INVALID (null pointers, sizes < 1, eps < 0), OOO_ERR_HIP.
+ * Errors: OOO_ERR_INVALID (null pointers, sizes < 1, eps < 0),
+ * OOO_ERR_UNSUPPORTED (dim not a multiple of 4 or above 8192), OOO_ERR_HIP.
  */
 int ooo_rmsnorm(const float* h, const void* weight, int32_t n_rows, int32_t dim, float eps, void* out,
                 void* stream);

@@ -25,70 +25,113 @@ __device__ __forceinline__ uint16_t f32_to_bf16_bits(float v) {
 }
 
 // ---------------------------------------------------------------- embedding
-// One block per node; a token outside [0, V) yields NaN rows (visible, not
-// silently clamped).
+// One block per node, 16-byte loads (8 bf16); a token outside [0, V)
+// yields NaN rows (visible, not silently clamped).  H % 8 == 0.
 __global__ __launch_bounds__(256) void embed_kernel(const uint16_t* __restrict__ table,
                                                     const int32_t* __restrict__ tokens, int H, int V,
                                                     float* __restrict__ h) {
   const int n = blockIdx.x;
   const int t = tokens[n];
   const bool ok = t >= 0 && t < V;
-  for (int c = threadIdx.x; c < H; c += blockDim.x)
-    h[(size_t)n * H + c] = ok ? bf16_bits_to_f32(table[(size_t)t * H + c]) : __builtin_nanf("");
+  for (int c = threadIdx.x * 8; c < H; c += 256 * 8) {
+    f32x4 lo = {__builtin_nanf(""), __builtin_nanf(""), __builtin_nanf(""), __builtin_nanf("")}, hi = lo;
+    if (ok) {
+      const u32x4 v = ld16(table + (size_t)t * H + c);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const f32x2_t f = {__uint_as_float(v[e] << 16), __uint_as_float(v[e] & 0xFFFF0000u)};
+        if (e < 2) {
+          lo[2 * e] = f[0];
+          lo[2 * e + 1] = f[1];
+        } else {
+          hi[2 * e - 4] = f[0];
+          hi[2 * e - 3] = f[1];
+        }
+      }
+    }
+    *reinterpret_cast<f32x4*>(h + (size_t)n * H + c) = lo;
+    *reinterpret_cast<f32x4*>(h + (size_t)n * H + c + 4) = hi;
+  }
 }
 
 // ------------------------------------------------------------------ RMSNorm
-// One block (256 threads) per row: sum of squares in fp32, then
-// out = h * (1 / sqrt(ss / H + eps)) * w rounded to bf16.
+// One block (256 threads) per row; the row (dim <= 8192, dim % 4 == 0) is
+// read once with all 16-byte loads issued up front and kept in registers:
+// sum of squares in fp32, then out = h * (1 / sqrt(ss / H + eps)) * w
+// rounded to bf16.
+constexpr int kNormVec = 8;  // float4 per thread
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ h, const uint16_t* __restrict__ w,
                                                       int H, float eps, uint16_t* __restrict__ out) {
   __shared__ float part[4];
   const int n = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const float* row = h + (size_t)n * H;
+  f32x4 v[kNormVec];
   float ss = 0.f;
-  for (int c = threadIdx.x; c < H; c += 256) {
-    const float v = row[c];
-    ss = __builtin_fmaf(v, v, ss);
+#pragma unroll
+  for (int i = 0; i < kNormVec; ++i) {
+    const int c = 4 * (threadIdx.x + 256 * i);
+    v[i] = c < H ? *reinterpret_cast<const f32x4*>(row + c) : f32x4{0.f, 0.f, 0.f, 0.f};
   }
+#pragma unroll
+  for (int i = 0; i < kNormVec; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) ss = __builtin_fmaf(v[i][e], v[i][e], ss);
   for (int off = 32; off > 0; off >>= 1) ss += shfl_xor_f(ss, off);
   if (lane == 0) part[wave] = ss;
   __syncthreads();
   const float tot = (part[0] + part[1]) + (part[2] + part[3]);
   const float r = 1.f / sqrtf(tot / (float)H + eps);
-  for (int c = threadIdx.x; c < H; c += 256)
-    out[(size_t)n * H + c] = f32_to_bf16_bits(row[c] * r * bf16_bits_to_f32(w[c]));
+#pragma unroll
+  for (int i = 0; i < kNormVec; ++i) {
+    const int c = 4 * (threadIdx.x + 256 * i);
+    if (c < H) {
+      const u32x2 wv = *reinterpret_cast<const u32x2*>(w + c);
+      u32x2 o;
+      o[0] = pack_bf16x2(v[i][0] * r * __uint_as_float(wv[0] << 16), v[i][1] * r * __uint_as_float(wv[0] & 0xFFFF0000u));
+      o[1] = pack_bf16x2(v[i][2] * r * __uint_as_float(wv[1] << 16), v[i][3] * r * __uint_as_float(wv[1] & 0xFFFF0000u));
+      *reinterpret_cast<u32x2*>(out + (size_t)n * H + c) = o;
+    }
+  }
 }
 
 // ------------------------------------------------------ QK norm and rotation
-// One block per node, one wave per head at a time.  Lane j < D/2 owns the
-// rotate-half pair (j, j + D/2) of every head, so its rotation angle
-// (P + depth[n]) * theta^(-2j/D) is computed once, in double precision, and
-// reused for all heads.  Heads [0, Hq) are queries, [Hq, Hq + Hkv) keys,
+// Block (node n, 16 heads), one wave per head: every load of the block is
+// issued at once.  Lane j < D/2 owns the rotate-half pair (j, j + D/2); its
+// rotation angle (P + depth[n]) * theta^(-2j/D) is formed in double
+// precision and reduced by multiples of 2 pi before a float sine/cosine.  Heads [0, Hq) are queries, [Hq, Hq + Hkv) keys,
 // [Hq + Hkv, Hq + 2 Hkv) values (copied to the cache unchanged).  A null norm
 // weight skips that norm (models without QK norms).
+// Rotation frequencies theta^(-2j/D), computed on the host in double.
+struct RopeFreq {
+  double f[64];
+};
+
 template <int D>
-__global__ __launch_bounds__(256) void qk_norm_rope_kernel(const uint16_t* __restrict__ qkv,
+__global__ __launch_bounds__(1024) void qk_norm_rope_kernel(const uint16_t* __restrict__ qkv,
                                                            const uint16_t* __restrict__ q_norm,
                                                            const uint16_t* __restrict__ k_norm, float eps,
-                                                           const int32_t* __restrict__ depth, int P, double theta,
+                                                           const int32_t* __restrict__ depth, int P, RopeFreq fr,
                                                            int Hq, int Hkv, uint16_t* __restrict__ q_out,
                                                            uint16_t* __restrict__ k_cache,
                                                            uint16_t* __restrict__ v_cache, long long cap) {
   constexpr int HALF = D / 2;
   const int n = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nh = Hq + 2 * Hkv;
+  const int hh = blockIdx.y * 16 + wave;  // this wave's head
+  if (hh >= nh) return;
   const uint16_t* src = qkv + (size_t)n * nh * D;
   const long long row = (long long)P + n;  // node n's cache row
   const bool act = lane < HALF;
   float cs = 1.f, sn = 0.f;
   if (act) {
-    const double ang = (double)(P + depth[n]) * pow(theta, -2.0 * (double)lane / (double)D);
-    double sd, cd;
-    sincos(ang, &sd, &cd);
-    cs = (float)cd;
-    sn = (float)sd;
+    // angle in double, reduced by multiples of 2 pi (two-term constant), so
+    // a float sine/cosine of a small argument finishes it
+    const double ang = (double)(P + depth[n]) * fr.f[lane];
+    const double k = rint(ang * 0.15915494309189535);
+    const double red = fma(-k, 2.4492935982947064e-16, fma(-k, 6.283185307179586, ang));
+    sincosf((float)red, &sn, &cs);
   }
-  for (int hh = wave; hh < nh; hh += 4) {
+  {
     const uint16_t* hr = src + (size_t)hh * D;
     if (hh >= Hq + Hkv) {
       const int g = hh - Hq - Hkv;
@@ -97,7 +140,7 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const uint16_t* __res
         dst[lane] = hr[lane];
         dst[lane + HALF] = hr[lane + HALF];
       }
-      continue;
+      return;
     }
     const bool is_q = hh < Hq;
     float a = act ? bf16_bits_to_f32(hr[lane]) : 0.f;
@@ -143,6 +186,7 @@ extern "C" int ooo_embed_rows(const void* table, const int32_t* tokens, int32_t 
                               int32_t vocab, float* h, void* stream) {
   OOO_REQUIRE(table && tokens && h, OOO_ERR_INVALID, "ooo_embed_rows: null pointer");
   OOO_REQUIRE(n_nodes >= 1 && hidden_dim >= 1 && vocab >= 1, OOO_ERR_INVALID, "ooo_embed_rows: sizes must be positive");
+  OOO_REQUIRE(hidden_dim % 8 == 0, OOO_ERR_UNSUPPORTED, "ooo_embed_rows: hidden_dim %% 8 != 0");
   embed_kernel<<<n_nodes, 256, 0, reinterpret_cast<hipStream_t>(stream)>>>((const uint16_t*)table, tokens, hidden_dim,
                                                                           vocab, h);
   const hipError_t e = hipGetLastError();
@@ -155,6 +199,8 @@ extern "C" int ooo_rmsnorm(const float* h, const void* weight, int32_t n_rows, i
   OOO_REQUIRE(h && weight && out, OOO_ERR_INVALID, "ooo_rmsnorm: null pointer");
   OOO_REQUIRE(n_rows >= 1 && dim >= 1, OOO_ERR_INVALID, "ooo_rmsnorm: sizes must be positive");
   OOO_REQUIRE(eps >= 0.f, OOO_ERR_INVALID, "ooo_rmsnorm: eps must be >= 0");
+  OOO_REQUIRE(dim % 4 == 0 && dim <= 4 * 256 * kNormVec, OOO_ERR_UNSUPPORTED,
+              "ooo_rmsnorm: dim %d not supported (a multiple of 4, at most %d)", dim, 4 * 256 * kNormVec);
   rmsnorm_kernel<<<n_rows, 256, 0, reinterpret_cast<hipStream_t>(stream)>>>(h, (const uint16_t*)weight, dim, eps,
                                                                            (uint16_t*)out);
   const hipError_t e = hipGetLastError();
@@ -176,14 +222,17 @@ extern "C" int ooo_qk_norm_rope(const void* qkv, const void* q_norm, const void*
   OOO_REQUIRE(head_dim == 64 || head_dim == 128, OOO_ERR_UNSUPPORTED,
               "ooo_qk_norm_rope: head_dim %d not supported (64 or 128)", head_dim);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  RopeFreq fr{};
+  for (int j = 0; j < head_dim / 2; ++j) fr.f[j] = pow(rope_theta, -2.0 * j / head_dim);
+  const dim3 grid(n_nodes, (n_q_heads + 2 * n_kv_heads + 15) / 16);
   if (head_dim == 128)
-    qk_norm_rope_kernel<128><<<n_nodes, 256, 0, st>>>((const uint16_t*)qkv, (const uint16_t*)q_norm,
-                                                      (const uint16_t*)k_norm, eps, depth, prefix_len, rope_theta,
+    qk_norm_rope_kernel<128><<<grid, 1024, 0, st>>>((const uint16_t*)qkv, (const uint16_t*)q_norm,
+                                                      (const uint16_t*)k_norm, eps, depth, prefix_len, fr,
                                                       n_q_heads, n_kv_heads, (uint16_t*)q_out, (uint16_t*)k_cache,
                                                       (uint16_t*)v_cache, cap);
   else
-    qk_norm_rope_kernel<64><<<n_nodes, 256, 0, st>>>((const uint16_t*)qkv, (const uint16_t*)q_norm,
-                                                     (const uint16_t*)k_norm, eps, depth, prefix_len, rope_theta,
+    qk_norm_rope_kernel<64><<<grid, 1024, 0, st>>>((const uint16_t*)qkv, (const uint16_t*)q_norm,
+                                                     (const uint16_t*)k_norm, eps, depth, prefix_len, fr,
                                                      n_q_heads, n_kv_heads, (uint16_t*)q_out, (uint16_t*)k_cache,
                                                      (uint16_t*)v_cache, cap);
   const hipError_t e = hipGetLastError();

@@ -151,6 +151,9 @@ def test_layer_entry_points_validate_on_host():
     assert L.ooo_embed_rows(fake, fake, 0, 64, 100, fake, None) == ooo.ERR_INVALID
     assert L.ooo_rmsnorm(fake, None, 4, 64, 1e-6, fake, None) == ooo.ERR_INVALID
     assert L.ooo_rmsnorm(fake, fake, 4, 64, -1.0, fake, None) == ooo.ERR_INVALID
+    assert L.ooo_rmsnorm(fake, fake, 4, 66, 1e-6, fake, None) == ooo.ERR_UNSUPPORTED
+    assert L.ooo_rmsnorm(fake, fake, 4, 8196, 1e-6, fake, None) == ooo.ERR_UNSUPPORTED
+    assert L.ooo_embed_rows(fake, fake, 4, 60, 100, fake, None) == ooo.ERR_UNSUPPORTED
     lin = lambda n=4, k=64, o=64, lay=ooo.W_PACKED, epi=ooo.EPI_STORE_F32, x=fake, ws=fake, wsb=1 << 30: \
         L.ooo_linear(x, fake, n, k, o, lay, epi, fake, ws, wsb, None)
     assert lin(n=0) == ooo.ERR_INVALID

@@ -67,7 +67,7 @@ def test_linear(N, K, O, packed):
     xd, wd = _dev_bf16(x), _dev_bf16(w)
     wl_ = ooo.linear_pack(wd) if packed else wd
     ref = f64(x) @ f64(w).T
-    ws = torch.empty(ooo.linear_workspace(N, K, O), dtype=torch.uint8, device=DEV)
+    ws = torch.zeros(ooo.linear_workspace(N, K, O), dtype=torch.uint8, device=DEV)
     y32 = torch.full((N, O), float("nan"), dtype=torch.float32, device=DEV)
     ooo.linear(xd, wl_, y32, ooo.EPI_STORE_F32, ws)
     assert gh.row_rel_err(y32.double().cpu().numpy(), ref) <= 1e-4
@@ -90,7 +90,8 @@ def test_linear(N, K, O, packed):
 
 
 @pytest.mark.parametrize("N,Hq,Hkv,D,P,norm", [(64, 32, 8, 128, 4096, True), (33, 4, 2, 64, 100, True),
-                                                (7, 40, 8, 128, 8192, False), (1, 2, 1, 64, 0, True)])
+                                                (7, 40, 8, 128, 8192, False), (1, 2, 1, 64, 0, True),
+                                                (16, 8, 2, 128, 45000, True)])
 def test_qk_norm_rope(N, Hq, Hkv, D, P, norm):
     """Queries, and the node keys/values in the cache rows P .. P + N - 1,
     match the reference norms and rotation at positions P + depth; every
