@@ -235,3 +235,60 @@ def test_model_verify_step(name, n_layers, depth):
         rows = slice(P, P + ref["L"] + 1)
         assert gh.row_rel_err(f64(kh[:, rows]), kcs[l][:, rows]) <= TOL
         assert gh.row_rel_err(f64(vh[:, rows]), vcs[l][:, rows]) <= TOL
+
+
+def test_model_chained_steps():
+    """Three verify steps in a row on the 2-layer model, each compacting the
+    accepted rows and moving the prefix on.  The GPU and the reference each
+    keep their own cache and see the same candidates (built from the
+    reference's own greedy continuation); the GPU commits exactly the
+    reference's tokens at every step, and its cache rows stay within
+    tolerance of the reference's."""
+    print("case model chained verify steps", flush=True)
+    import dataclasses
+    cfg = dataclasses.replace(mw.MODEL_CONFIGS["small-model"], cap=160)
+    seed = 5
+    lws, emb, fin, lm, ref_layers, shp = _model(cfg, seed, cfg.n_layers)
+    P = cfg.prefix_len
+    kv = [mw.prefix_kv(cfg, seed, l) for l in range(cfg.n_layers)]
+    kcs = [np.concatenate([f64(k), np.zeros((cfg.n_kv_heads, cfg.cap - k.shape[1], cfg.head_dim))], axis=1)
+           if k.shape[1] < cfg.cap else f64(k) for k, _ in kv]
+    vcs = [np.concatenate([f64(v), np.zeros((cfg.n_kv_heads, cfg.cap - v.shape[1], cfg.head_dim))], axis=1)
+           if v.shape[1] < cfg.cap else f64(v) for _, v in kv]
+    runner = ModelRunner(cfg, lws, emb, fin, lm, DEV)
+    kc = torch.zeros(cfg.n_layers, cfg.n_kv_heads, cfg.cap, cfg.head_dim, dtype=torch.bfloat16, device=DEV)
+    vc = torch.zeros_like(kc)
+    for l, (k, v) in enumerate(kv):
+        kc[l, :, :k.shape[1]] = _dev_bf16(k)
+        vc[l, :, :v.shape[1]] = _dev_bf16(v)
+    toks = mw.random_tokens(cfg, seed, 200)
+    root = toks[0]
+    for step, depth in enumerate([3, 0, 4]):
+        chain = _greedy_chain(cfg, shp, ref_layers, emb, fin, lm, kcs, vcs, root, P, depth)
+        wrong = (chain[depth] + 1) % cfg.vocab
+        o = 10 * step
+        # other lanes: random tokens whose first token is not the greedy one,
+        # and (when depth >= 1) a lane sharing the greedy first token only
+        other = [t if t != chain[0] else (t + 1) % cfg.vocab for t in toks[o + 3:o + 7]]
+        cands = [chain[:depth] + [wrong] + toks[o + 1:o + 3], other]
+        if depth >= 1:
+            cands.append(chain[:1] + [(chain[1] + 2) % cfg.vocab] + toks[o + 7:o + 9])
+        ref = om.verify_step(root, cands, cfg.max_nodes, cfg.max_depth, P, _Widen(emb), ref_layers, f64(fin),
+                             _Widen(lm), shp, kcs, vcs)
+        assert ref["L"] == depth
+        offs = np.zeros(len(cands) + 1, np.int32)
+        for i, c in enumerate(cands):
+            offs[i + 1] = offs[i] + len(c)
+        runner.pack(root, np.array([t for c in cands for t in c], np.int32), offs)
+        runner.device_step(kc, vc, P)
+        torch.cuda.synchronize()
+        res = runner.result()
+        assert res.L == ref["L"] and res.bonus == ref["bonus"], (step, res.L, ref["L"])
+        assert np.array_equal(res.path, ref["path"])
+        newP = P + res.L + 1
+        for l in range(cfg.n_layers):
+            kh, vh = gh.to_host(kc[l], "bf16"), gh.to_host(vc[l], "bf16")
+            assert gh.row_rel_err(f64(kh[:, :newP]), kcs[l][:, :newP]) <= TOL
+            assert gh.row_rel_err(f64(vh[:, :newP]), vcs[l][:, :newP]) <= TOL
+        P = newP
+        root = res.bonus
