@@ -701,7 +701,12 @@ template <int D, int SMAX>
 __global__ __launch_bounds__(256) void tree_attn_combine_kernel(AttnArgs a) {
   constexpr int NP = D / 16;  // group pairs per lane
   const int lane = threadIdx.x & 63;
-  const int wv = blockIdx.x * 4 + (threadIdx.x >> 6);
+  // Same XCD-aware order as the main kernel: the blocks that share
+  // blockIdx % 8 take one contiguous range of (KV head, row block), the
+  // range whose partials that XCD wrote, so the loads hit its L2.
+  int b = blockIdx.x;
+  if (gridDim.x % 8 == 0) b = (b % 8) * (gridDim.x / 8) + b / 8;
+  const int wv = b * 4 + (threadIdx.x >> 6);
   const int nblk = a.Mpad / 32;
   if (wv >= a.Hkv * nblk * NP) return;
   const int k = wv % NP, blk = (wv / NP) % nblk, g = wv / (NP * nblk);
@@ -717,8 +722,8 @@ __global__ __launch_bounds__(256) void tree_attn_combine_kernel(AttnArgs a) {
 #pragma unroll
   for (int s = 0; s < SMAX; ++s) {
     const int sc = min(s, a.splits - 1);
-    ml[s] = __builtin_nontemporal_load(pml + sc * split_ml);  // read once: do not keep in cache
-    o[s] = __builtin_nontemporal_load(po + sc * split_o);
+    ml[s] = pml[sc * split_ml];
+    o[s] = po[sc * split_o];
   }
   float m = -INFINITY;
 #pragma unroll
