@@ -154,6 +154,11 @@ int ooo_hint_merge(const int32_t* bank, int64_t bank_len, int32_t eos_token, con
  *              the committed prefix, row P + i holds node i's key/value
  *   cap        rows per KV head; P + n_nodes <= cap
  *   prefix_len P >= 0
+ *   prefix_len_dev  NULL, or a device int32 holding the prefix length to use
+ *              at run time (a decode loop that replays one captured step
+ *              while P grows); prefix_len is then its upper bound, used for
+ *              validation and planning, and a device value outside
+ *              [0, prefix_len] is clamped into it
  *   anc_mask   [n_nodes][mask_words] from ooo_pack_tree (device copy)
  *   scale      score scale, normally 1/sqrt(head_dim)
  *   out        [n_nodes][n_q_heads][head_dim], same dtype; must not alias
@@ -170,7 +175,8 @@ int ooo_hint_merge(const int32_t* bank, int64_t bank_len, int32_t eos_token, con
 size_t ooo_tree_attn_workspace(int32_t n_nodes, int32_t n_q_heads, int32_t n_kv_heads,
                                int32_t head_dim, int32_t prefix_len, ooo_dtype dt);
 int ooo_tree_attn(const void* q, const void* k_cache, const void* v_cache, int64_t cap,
-                  int32_t prefix_len, int32_t n_nodes, const uint64_t* anc_mask,
+                  int32_t prefix_len, const int32_t* prefix_len_dev, int32_t n_nodes,
+                  const uint64_t* anc_mask,
                   int32_t mask_words, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
                   float scale, ooo_dtype dt, void* out, void* workspace, size_t ws_bytes,
                   void* stream);
@@ -255,6 +261,11 @@ int ooo_accept(const int32_t* token, const int32_t* parent, const int32_t* depth
  * DEVICE pointers.
  *   k_cache, v_cache   [n_layers][n_kv_heads][cap][head_dim], updated in place
  *   prefix_len         P, the committed length before this step
+ *   prefix_len_dev     NULL, or a device int32 holding the prefix length to
+ *                      use at run time (a decode loop that replays one
+ *                      captured step while P grows); prefix_len is then its
+ *                      upper bound, used for validation and planning, and a
+ *                      device value outside [0, prefix_len] is clamped into it
  *   n_nodes            trie size of the step; node rows are [P, P + n_nodes)
  *   path, accept_len   outputs of ooo_accept (read on the device, so no host
  *                      synchronisation is needed in between)
@@ -272,8 +283,8 @@ int ooo_accept(const int32_t* token, const int32_t* parent, const int32_t* depth
  */
 int ooo_kv_compact(void* k_cache, void* v_cache, int32_t n_layers, int32_t n_kv_heads,
                    int64_t cap, int32_t head_dim, ooo_dtype dt, int32_t prefix_len,
-                   int32_t n_nodes, const int32_t* path, const int32_t* accept_len,
-                   int32_t path_cap, void* stream);
+                   const int32_t* prefix_len_dev, int32_t n_nodes, const int32_t* path,
+                   const int32_t* accept_len, int32_t path_cap, void* stream);
 
 /*
  * ooo_embed_rows - residual rows of the trie's tokens (the input of the
@@ -355,6 +366,8 @@ int ooo_linear(const void* x, const void* weight, int32_t n_rows, int32_t in_dim
  *   q_norm, k_norm   [head_dim] bf16 per-head RMSNorm weights of q and k
  *             (Qwen3), or NULL for no norm
  *   depth     [n_nodes] int32 (the packed trie's depths)
+ *   prefix_len P; prefix_len_dev as for ooo_tree_attn (NULL, or the device
+ *             prefix length that prefix_len bounds)
  *   q_out     [n_nodes][n_q_heads][head_dim] bf16
  *   k_cache, v_cache   one layer, [n_kv_heads][cap][head_dim] bf16; rows
  *             P .. P + n_nodes - 1 are written
@@ -366,7 +379,8 @@ int ooo_linear(const void* x, const void* weight, int32_t n_rows, int32_t in_dim
  * OOO_ERR_HIP.
  */
 int ooo_qk_norm_rope(const void* qkv, const void* q_norm, const void* k_norm, float eps,
-                     const int32_t* depth, int32_t n_nodes, int32_t prefix_len, double rope_theta,
+                     const int32_t* depth, int32_t n_nodes, int32_t prefix_len,
+                     const int32_t* prefix_len_dev, double rope_theta,
                      int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, void* q_out,
                      void* k_cache, void* v_cache, int64_t cap, void* stream);
 

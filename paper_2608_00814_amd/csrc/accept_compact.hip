@@ -81,7 +81,8 @@ __global__ __launch_bounds__(1024) void accept_kernel(const int32_t* __restrict_
 }
 
 __global__ __launch_bounds__(256) void kv_compact_kernel(uint8_t* __restrict__ k, uint8_t* __restrict__ v,
-                                                         int Hkv, long long cap, int row_bytes, int P, int N,
+                                                         int Hkv, long long cap, int row_bytes, int P,
+                                                         const int32_t* __restrict__ P_dev, int N,
                                                          const int32_t* __restrict__ path,
                                                          const int32_t* __restrict__ accept_len, int path_cap) {
   const int slice = blockIdx.x;  // (layer * Hkv + head) * 2 + (K or V)
@@ -100,6 +101,7 @@ __global__ __launch_bounds__(256) void kv_compact_kernel(uint8_t* __restrict__ k
   }
   int L = *accept_len;
   if (L > path_cap - 1) L = path_cap - 1;
+  if (P_dev) P = min(max(*P_dev, 0), P);  // device prefix, bounded by the launch value
   for (int d0 = 1; d0 <= L; d0 += rows_per_pass) {
     u32x4 buf[R];
     int dst[R];
@@ -153,7 +155,8 @@ extern "C" int ooo_accept(const int32_t* token, const int32_t* parent, const int
 }
 
 extern "C" int ooo_kv_compact(void* k_cache, void* v_cache, int32_t n_layers, int32_t n_kv_heads, int64_t cap,
-                              int32_t head_dim, ooo_dtype dt, int32_t prefix_len, int32_t n_nodes,
+                              int32_t head_dim, ooo_dtype dt, int32_t prefix_len, const int32_t* prefix_len_dev,
+                              int32_t n_nodes,
                               const int32_t* path, const int32_t* accept_len, int32_t path_cap, void* stream) {
   OOO_REQUIRE(k_cache && v_cache && path && accept_len, OOO_ERR_INVALID, "ooo_kv_compact: null pointer");
   OOO_REQUIRE(n_layers >= 1 && n_kv_heads >= 1 && head_dim >= 1 && n_nodes >= 1 && path_cap >= 1,
@@ -171,10 +174,10 @@ extern "C" int ooo_kv_compact(void* k_cache, void* v_cache, int32_t n_layers, in
   const dim3 grid(n_layers * n_kv_heads * 2);
   if (esz == 2)
     kv_compact_kernel<<<grid, 256, 0, st>>>((uint8_t*)k_cache, (uint8_t*)v_cache, n_kv_heads, cap, row_bytes,
-                                                prefix_len, n_nodes, path, accept_len, path_cap);
+                                                prefix_len, prefix_len_dev, n_nodes, path, accept_len, path_cap);
   else
     kv_compact_kernel<<<grid, 256, 0, st>>>((uint8_t*)k_cache, (uint8_t*)v_cache, n_kv_heads, cap, row_bytes,
-                                                prefix_len, n_nodes, path, accept_len, path_cap);
+                                                prefix_len, prefix_len_dev, n_nodes, path, accept_len, path_cap);
   const hipError_t e = hipGetLastError();
   OOO_REQUIRE(e == hipSuccess, OOO_ERR_HIP, "ooo_kv_compact: launch failed: %s", hipGetErrorString(e));
   return ooo::ok();

@@ -110,11 +110,13 @@ template <int D>
 __global__ __launch_bounds__(1024) void qk_norm_rope_kernel(const uint16_t* __restrict__ qkv,
                                                            const uint16_t* __restrict__ q_norm,
                                                            const uint16_t* __restrict__ k_norm, float eps,
-                                                           const int32_t* __restrict__ depth, int P, RopeFreq fr,
+                                                           const int32_t* __restrict__ depth, int P,
+                                                           const int32_t* __restrict__ P_dev, RopeFreq fr,
                                                            int Hq, int Hkv, uint16_t* __restrict__ q_out,
                                                            uint16_t* __restrict__ k_cache,
                                                            uint16_t* __restrict__ v_cache, long long cap) {
   constexpr int HALF = D / 2;
+  if (P_dev) P = min(max(*P_dev, 0), P);  // device prefix, bounded by the launch value
   const int n = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nh = Hq + 2 * Hkv;
   const int hh = blockIdx.y * 16 + wave;  // this wave's head
@@ -209,7 +211,8 @@ extern "C" int ooo_rmsnorm(const float* h, const void* weight, int32_t n_rows, i
 }
 
 extern "C" int ooo_qk_norm_rope(const void* qkv, const void* q_norm, const void* k_norm, float eps,
-                                const int32_t* depth, int32_t n_nodes, int32_t prefix_len, double rope_theta,
+                                const int32_t* depth, int32_t n_nodes, int32_t prefix_len,
+                                const int32_t* prefix_len_dev, double rope_theta,
                                 int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, void* q_out,
                                 void* k_cache, void* v_cache, int64_t cap, void* stream) {
   OOO_REQUIRE(qkv && depth && q_out && k_cache && v_cache, OOO_ERR_INVALID, "ooo_qk_norm_rope: null pointer");
@@ -227,12 +230,12 @@ extern "C" int ooo_qk_norm_rope(const void* qkv, const void* q_norm, const void*
   const dim3 grid(n_nodes, (n_q_heads + 2 * n_kv_heads + 15) / 16);
   if (head_dim == 128)
     qk_norm_rope_kernel<128><<<grid, 1024, 0, st>>>((const uint16_t*)qkv, (const uint16_t*)q_norm,
-                                                      (const uint16_t*)k_norm, eps, depth, prefix_len, fr,
+                                                      (const uint16_t*)k_norm, eps, depth, prefix_len, prefix_len_dev, fr,
                                                       n_q_heads, n_kv_heads, (uint16_t*)q_out, (uint16_t*)k_cache,
                                                       (uint16_t*)v_cache, cap);
   else
     qk_norm_rope_kernel<64><<<grid, 1024, 0, st>>>((const uint16_t*)qkv, (const uint16_t*)q_norm,
-                                                     (const uint16_t*)k_norm, eps, depth, prefix_len, fr,
+                                                     (const uint16_t*)k_norm, eps, depth, prefix_len, prefix_len_dev, fr,
                                                      n_q_heads, n_kv_heads, (uint16_t*)q_out, (uint16_t*)k_cache,
                                                      (uint16_t*)v_cache, cap);
   const hipError_t e = hipGetLastError();

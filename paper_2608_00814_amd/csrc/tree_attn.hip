@@ -55,6 +55,7 @@ struct AttnArgs {
   uint32_t* part_o;  // fp16 normalised partial outputs (fragment order)
   float* part_ml;    // per partial row: max, sum, scale, unused
   int splits, row_blocks, Mpad, tiles_prefix, tiles_total;
+  const int* P_dev;  // null, or the prefix length in device memory (P bounds it)
 };
 
 // swap bits 2 and 3: the K row a lane loads so that S^T lands with eight
@@ -180,9 +181,17 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
   w /= a.splits;
   const int rb = w % a.row_blocks;
   const int g = w / a.row_blocks;
-  const int t_begin = (int)((long long)s * a.tiles_total / a.splits);
-  const int t_end = (int)((long long)(s + 1) * a.tiles_total / a.splits);
-  const int ntiles = t_end - t_begin;  // >= 1 because splits <= tiles
+  // The prefix length is the launch value or, for replays of one captured
+  // step at a growing prefix, the value in device memory (clamped to the
+  // launch value, which the plan and the validation used).
+  const int P = a.P_dev ? __builtin_amdgcn_readfirstlane(min(max(*a.P_dev, 0), a.P)) : a.P;
+  const int tiles_prefix = (P + kTile - 1) / kTile;
+  const int tiles_total = tiles_prefix + (a.N + kTile - 1) / kTile;
+  const int t_begin = (int)((long long)s * tiles_total / a.splits);
+  const int t_end = (int)((long long)(s + 1) * tiles_total / a.splits);
+  // >= 1 when the plan's prefix is the actual one (splits <= tiles); a
+  // shorter device prefix can leave a split empty (handled below)
+  const int ntiles = t_end - t_begin;
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint32_t wave_u = __builtin_amdgcn_readfirstlane(wave);
@@ -197,6 +206,20 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
   const uint16_t* const kg = a.k + (size_t)g * a.cap * D;
   const uint16_t* const vg = a.v + (size_t)g * a.cap * D;
 
+  if (ntiles <= 0) {
+    // Empty split (only with a device prefix shorter than the plan's; then
+    // splits > 1): a partial with no allowed key, zero weight in the merge.
+    if (kh0 != 0 || !row_ok) return;
+    const size_t blk = ((size_t)s * a.Hkv + g) * (a.Mpad / 32) + (row >> 5);
+    u32x4* po = reinterpret_cast<u32x4*>(a.part_o) + blk * (R::GPL / 2) * 64 + lane;
+#pragma unroll
+    for (int k = 0; k < R::GPL / 2; ++k) po[k * 64] = u32x4{0u, 0u, 0u, 0u};
+    if (u == 0)
+      *reinterpret_cast<f32x4*>(a.part_ml + (((size_t)s * a.Hkv + g) * a.Mpad + row) * 4) =
+          f32x4{-INFINITY, 0.f, 1.f, 0.f};
+    return;
+  }
+
   // Q^T fragments (B operand of S^T = K Q^T): row c, k = 16dk + 8u .. +8.
   // The key-split kernel stages Q through LDS instead (below).
   bf16x8 qf[D / 16];
@@ -207,12 +230,12 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
   }
 
   auto tile_rows = [&](int t, int& row0, int& limit) OOO_INLINE {
-    if (t < a.tiles_prefix) {
+    if (t < tiles_prefix) {
       row0 = t * kTile;
-      limit = a.P;
+      limit = P;
     } else {
-      row0 = a.P + (t - a.tiles_prefix) * kTile;
-      limit = a.P + a.N;
+      row0 = P + (t - tiles_prefix) * kTile;
+      limit = P + a.N;
     }
   };
   // DMA instruction j of a matrix copies rows RPI*j .. +RPI: lane = (row
@@ -373,10 +396,10 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
   auto apply_mask = [&](int t, f32x16 (&acc)[NH]) OOO_INLINE {
     int row0, limit;
     tile_rows(t, row0, limit);
-    const bool tree = t >= a.tiles_prefix;
+    const bool tree = t >= tiles_prefix;
     if (tree || row0 + kTile > limit) {
       const uint64_t mw =
-          !tree ? ~0ull : SPLIT ? mwords[(rg * 32 + c) * a.W + (t - a.tiles_prefix)] : mrow[t - a.tiles_prefix];
+          !tree ? ~0ull : SPLIT ? mwords[(rg * 32 + c) * a.W + (t - tiles_prefix)] : mrow[t - tiles_prefix];
 #pragma unroll
       for (int hf = 0; hf < NH; ++hf)
 #pragma unroll
@@ -560,7 +583,7 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
         __builtin_amdgcn_sched_barrier(0);
         int row0, limit;
         tile_rows(t_begin + i + 1, row0, limit);
-        if (t_begin + i + 1 >= a.tiles_prefix || row0 + kTile > limit) {
+        if (t_begin + i + 1 >= tiles_prefix || row0 + kTile > limit) {
           apply_mask(t_begin + i + 1, snxt);
           mx = row_max(snxt);
         }
@@ -759,9 +782,11 @@ __global__ __launch_bounds__(256) void tree_attn_combine_kernel(AttnArgs a) {
 // an online softmax; each lane owns head_dim/64 columns.
 template <int D>
 __global__ __launch_bounds__(64) void tree_attn_f32_kernel(const float* q, const float* k, const float* v,
-                                                           long long cap, int P, int N, const uint64_t* mask,
-                                                           int W, int Hq, int Hkv, float scale, float* out) {
+                                                           long long cap, int P, const int* P_dev, int N,
+                                                           const uint64_t* mask, int W, int Hq, int Hkv, float scale,
+                                                           float* out) {
   constexpr int C = D / 64;
+  if (P_dev) P = min(max(*P_dev, 0), P);
   const int node = blockIdx.x / Hq, head = blockIdx.x % Hq;
   const int g = head / (Hq / Hkv);
   const int lane = threadIdx.x;
@@ -839,7 +864,8 @@ extern "C" size_t ooo_tree_attn_workspace(int32_t n_nodes, int32_t n_q_heads, in
 }
 
 extern "C" int ooo_tree_attn(const void* q, const void* k_cache, const void* v_cache, int64_t cap,
-                             int32_t prefix_len, int32_t n_nodes, const uint64_t* anc_mask,
+                             int32_t prefix_len, const int32_t* prefix_len_dev, int32_t n_nodes,
+                             const uint64_t* anc_mask,
                              int32_t mask_words, int32_t n_q_heads, int32_t n_kv_heads,
                              int32_t head_dim, float scale, ooo_dtype dt, void* out, void* workspace,
                              size_t ws_bytes, void* stream) {
@@ -866,12 +892,12 @@ extern "C" int ooo_tree_attn(const void* q, const void* k_cache, const void* v_c
     const dim3 grid(n_nodes * n_q_heads);
     if (head_dim == 64)
       tree_attn_f32_kernel<64><<<grid, 64, 0, st>>>((const float*)q, (const float*)k_cache, (const float*)v_cache,
-                                                    cap, prefix_len, n_nodes, anc_mask, mask_words, n_q_heads,
-                                                    n_kv_heads, scale, (float*)out);
+                                                    cap, prefix_len, prefix_len_dev, n_nodes, anc_mask, mask_words,
+                                                    n_q_heads, n_kv_heads, scale, (float*)out);
     else
       tree_attn_f32_kernel<128><<<grid, 64, 0, st>>>((const float*)q, (const float*)k_cache, (const float*)v_cache,
-                                                     cap, prefix_len, n_nodes, anc_mask, mask_words, n_q_heads,
-                                                     n_kv_heads, scale, (float*)out);
+                                                     cap, prefix_len, prefix_len_dev, n_nodes, anc_mask,
+                                                     mask_words, n_q_heads, n_kv_heads, scale, (float*)out);
   } else {
     const Plan p = make_plan(n_nodes, n_q_heads, n_kv_heads, head_dim, prefix_len, dt);
     OOO_REQUIRE(ws_bytes >= p.ws_bytes && (p.ws_bytes == 0 || workspace), OOO_ERR_CAPACITY,
@@ -882,6 +908,7 @@ extern "C" int ooo_tree_attn(const void* q, const void* k_cache, const void* v_c
     a.v = (const uint16_t*)v_cache;
     a.cap = cap;
     a.P = prefix_len;
+    a.P_dev = prefix_len_dev;
     a.N = n_nodes;
     a.mask = anc_mask;
     a.W = mask_words;

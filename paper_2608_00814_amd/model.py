@@ -82,10 +82,12 @@ class ModelRunner:
         return self.vr.pack(root_token, cand_tokens, cand_offsets, keep=keep)
 
     # -- device -------------------------------------------------------------
-    def forward(self, k_cache: torch.Tensor, v_cache: torch.Tensor, prefix_len: int) -> None:
+    def forward(self, k_cache: torch.Tensor, v_cache: torch.Tensor, prefix_len: int, prefix_dev=None) -> None:
         """Decoder layers over the packed trie (already uploaded): leaves the
         LM-head input rows in ``self.xf`` and each layer's attention output
-        in ``self.vr.out``; node k/v rows go to the caches' rows [P, P + N)."""
+        in ``self.vr.out``; node k/v rows go to the caches' rows [P, P + N).
+        With ``prefix_dev`` (an int32 device scalar) the kernels read P from
+        it and ``prefix_len`` is only its upper bound."""
         cfg, vr = self.cfg, self.vr
         N, P = vr.n_nodes, prefix_len
         vr.ensure_workspace(P)  # allocates only for a larger shape than seen before (never inside a capture)
@@ -95,8 +97,8 @@ class ModelRunner:
             ooo.rmsnorm(self.h, w["in_norm"], cfg.eps, self.x, n_rows=N)
             ooo.linear(self.x, w["w_qkv"], self.qkv, ooo.EPI_STORE_BF16, ws, n_rows=N)
             ooo.qk_norm_rope(self.qkv, w["q_norm"], w["k_norm"], cfg.eps, vr.depth, N, P, cfg.rope_theta,
-                             cfg.n_q_heads, cfg.n_kv_heads, self.q, k_cache[l], v_cache[l])
-            vr.attention(l, self.q, k_cache[l], v_cache[l], P)
+                             cfg.n_q_heads, cfg.n_kv_heads, self.q, k_cache[l], v_cache[l], prefix_dev=prefix_dev)
+            vr.attention(l, self.q, k_cache[l], v_cache[l], P, prefix_dev=prefix_dev)
             o = vr.out[l].view(cfg.max_nodes, cfg.n_q_heads * cfg.head_dim)
             ooo.linear(o, w["w_o"], self.h, ooo.EPI_ADD_F32, ws, n_rows=N)
             ooo.rmsnorm(self.h, w["post_norm"], cfg.eps, self.x, n_rows=N)
@@ -105,15 +107,15 @@ class ModelRunner:
         ooo.rmsnorm(self.h, self.final_norm, cfg.eps, self.xf, n_rows=N)
 
     def device_step(self, k_cache: torch.Tensor, v_cache: torch.Tensor, prefix_len: int,
-                    logits: Optional[torch.Tensor] = None, compact: bool = True) -> None:
+                    logits: Optional[torch.Tensor] = None, compact: bool = True, prefix_dev=None) -> None:
         """Everything after packing, enqueued on the current stream."""
         vr = self.vr
         vr.upload_tree()
-        self.forward(k_cache, v_cache, prefix_len)
+        self.forward(k_cache, v_cache, prefix_len, prefix_dev)
         vr.lm_head(self.xf, logits)
         vr.accept()
         if compact:
-            vr.compact(k_cache, v_cache, prefix_len)
+            vr.compact(k_cache, v_cache, prefix_len, prefix_dev=prefix_dev)
         vr.download()
 
     def result(self):

@@ -38,7 +38,7 @@ SIGNATURES = {
     "ooo_hint_merge": (ctypes.c_int, [_c_i32p, _i64, _i32, _c_i32p, _i32, _i32, _i32, _c_i32p, _c_i32p, _i32,
                                       _i32, _c_i32p, _i64, _c_i32p, _c_i32p, _c_i32p, _c_i32p]),
     "ooo_tree_attn_workspace": (_sz, [_i32, _i32, _i32, _i32, _i32, ctypes.c_int]),
-    "ooo_tree_attn": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _i32, _vp, _i32, _i32, _i32, _i32,
+    "ooo_tree_attn": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _vp, _i32, _vp, _i32, _i32, _i32, _i32,
                                      ctypes.c_float, ctypes.c_int, _vp, _vp, _sz, _vp]),
     "ooo_lmhead_workspace": (_sz, [_i32, _i32, _i32, ctypes.c_int]),
     "ooo_lmhead_packed_bytes": (_sz, [_i32, _i32, ctypes.c_int]),
@@ -46,7 +46,7 @@ SIGNATURES = {
     "ooo_lmhead_argmax": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, ctypes.c_int, _i32, _vp, _vp, _vp, _vp, _sz,
                                          _vp]),
     "ooo_accept": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i32, _vp, _i32, _i32, _vp, _vp, _vp, _vp]),
-    "ooo_kv_compact": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i64, _i32, ctypes.c_int, _i32, _i32, _vp, _vp,
+    "ooo_kv_compact": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i64, _i32, ctypes.c_int, _i32, _vp, _i32, _vp, _vp,
                                       _i32, _vp]),
     "ooo_embed_rows": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _vp, _vp]),
     "ooo_rmsnorm": (ctypes.c_int, [_vp, _vp, _i32, _i32, ctypes.c_float, _vp, _vp]),
@@ -54,7 +54,7 @@ SIGNATURES = {
     "ooo_linear_packed_bytes": (_sz, [_i32, _i32]),
     "ooo_linear_pack": (ctypes.c_int, [_vp, _i32, _i32, _vp, _sz, _vp]),
     "ooo_linear": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, ctypes.c_int, _vp, _vp, _sz, _vp]),
-    "ooo_qk_norm_rope": (ctypes.c_int, [_vp, _vp, _vp, ctypes.c_float, _vp, _i32, _i32, ctypes.c_double, _i32,
+    "ooo_qk_norm_rope": (ctypes.c_int, [_vp, _vp, _vp, ctypes.c_float, _vp, _i32, _i32, _vp, ctypes.c_double, _i32,
                                         _i32, _i32, _vp, _vp, _vp, _i64, _vp]),
     "ooo_swiglu": (ctypes.c_int, [_vp, _i32, _i32, _vp, _vp]),
 }
@@ -108,6 +108,17 @@ def dtype_code(t) -> int:
 
 def _ptr(t) -> Optional[int]:
     return None if t is None else t.data_ptr()
+
+
+def _prefix_ptr(t) -> Optional[int]:
+    """Device prefix length: None, or an int32 device tensor (its first element)."""
+    if t is None:
+        return None
+    import torch
+
+    if not t.is_cuda or t.dtype != torch.int32 or t.numel() < 1:
+        raise ValueError("prefix_dev must be an int32 device tensor with at least one element")
+    return t.data_ptr()
 
 
 def _dev(t, name: str, contiguous: bool = True):
@@ -245,15 +256,18 @@ def tree_attn_workspace(n_nodes: int, n_q_heads: int, n_kv_heads: int, head_dim:
 
 
 def tree_attn(q, k_cache, v_cache, prefix_len: int, n_nodes: int, anc_mask, n_q_heads: int, n_kv_heads: int,
-              scale: float, out, workspace=None, stream=None) -> None:
+              scale: float, out, workspace=None, stream=None, prefix_dev=None) -> None:
     """q [N][Hq][D]; k_cache/v_cache one layer [Hkv][cap][D]; anc_mask
-    [N][W] int64/uint64 device tensor; out [N][Hq][D]."""
+    [N][W] int64/uint64 device tensor; out [N][Hq][D].  ``prefix_dev``: an
+    int32 device tensor whose first element is the prefix length used at run
+    time (``prefix_len`` bounds it), or None."""
     for t, nm in ((q, "q"), (k_cache, "k_cache"), (v_cache, "v_cache"), (anc_mask, "anc_mask"), (out, "out")):
         _dev(t, nm)
     Hkv, cap, D = k_cache.shape
     W = anc_mask.shape[-1]
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    _check(lib().ooo_tree_attn(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), cap, prefix_len, n_nodes,
+    _check(lib().ooo_tree_attn(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), cap, prefix_len,
+                               _prefix_ptr(prefix_dev), n_nodes,
                                anc_mask.data_ptr(), W, n_q_heads, n_kv_heads, D, float(scale), dtype_code(q),
                                out.data_ptr(), _ptr(workspace), ws_bytes, _stream(stream)))
 
@@ -319,13 +333,16 @@ def accept(token, parent, depth, anc_mask, argmax_ids, n_nodes: int, path, accep
                             bonus_token.data_ptr(), _stream(stream)))
 
 
-def kv_compact(k_cache, v_cache, prefix_len: int, n_nodes: int, path, accept_len, stream=None) -> None:
-    """k_cache/v_cache [L][Hkv][cap][D] contiguous, updated in place."""
+def kv_compact(k_cache, v_cache, prefix_len: int, n_nodes: int, path, accept_len, stream=None,
+               prefix_dev=None) -> None:
+    """k_cache/v_cache [L][Hkv][cap][D] contiguous, updated in place;
+    ``prefix_dev`` as for ``tree_attn``."""
     for t, nm in ((k_cache, "k_cache"), (v_cache, "v_cache"), (path, "path"), (accept_len, "accept_len")):
         _dev(t, nm)
     L, Hkv, cap, D = k_cache.shape
     _check(lib().ooo_kv_compact(k_cache.data_ptr(), v_cache.data_ptr(), L, Hkv, cap, D, dtype_code(k_cache),
-                                prefix_len, n_nodes, path.data_ptr(), accept_len.data_ptr(), path.numel(),
+                                prefix_len, _prefix_ptr(prefix_dev), n_nodes, path.data_ptr(), accept_len.data_ptr(),
+                                path.numel(),
                                 _stream(stream)))
 
 
@@ -393,14 +410,16 @@ def linear(x, weight, out, epilogue: int, workspace, n_rows: Optional[int] = Non
 
 
 def qk_norm_rope(qkv, q_norm, k_norm, eps: float, depth, n_nodes: int, prefix_len: int, rope_theta: float,
-                 n_q_heads: int, n_kv_heads: int, q_out, k_cache, v_cache, stream=None) -> None:
+                 n_q_heads: int, n_kv_heads: int, q_out, k_cache, v_cache, stream=None, prefix_dev=None) -> None:
     """qkv [N][(Hq + 2 Hkv) D] bf16; q_norm/k_norm [D] bf16 or None; depth
-    [>= N] int32; q_out [N][Hq][D]; k_cache/v_cache one layer [Hkv][cap][D]."""
+    [>= N] int32; q_out [N][Hq][D]; k_cache/v_cache one layer [Hkv][cap][D];
+    ``prefix_dev`` as for ``tree_attn``."""
     for t, nm in ((qkv, "qkv"), (depth, "depth"), (q_out, "q_out"), (k_cache, "k_cache"), (v_cache, "v_cache")):
         _dev(t, nm)
     _, cap, D = k_cache.shape
     _check(lib().ooo_qk_norm_rope(qkv.data_ptr(), _ptr(q_norm), _ptr(k_norm), float(eps), depth.data_ptr(), n_nodes,
-                                  prefix_len, float(rope_theta), n_q_heads, n_kv_heads, D, q_out.data_ptr(),
+                                  prefix_len, _prefix_ptr(prefix_dev), float(rope_theta), n_q_heads, n_kv_heads, D,
+                                  q_out.data_ptr(),
                                   k_cache.data_ptr(), v_cache.data_ptr(), cap, _stream(stream)))
 
 

@@ -49,8 +49,10 @@ class VerifyRunner:
         self.code = ooo.BF16 if dtype == torch.bfloat16 else ooo.F32
         dev = self.device
         self.path_cap = max_depth + 1
-        # trie on the device, filled from pinned host staging
-        self.h_tree = torch.zeros(3 * max_nodes + 2 * max_nodes * self.W, dtype=torch.int32).pin_memory()
+        # trie on the device, filled from pinned host staging; the last
+        # entries are a header (the prefix length the step runs at, read on
+        # the device when one captured step is replayed at a growing prefix)
+        self.h_tree = torch.zeros(3 * max_nodes + 2 * max_nodes * self.W + 4, dtype=torch.int32).pin_memory()
         self.d_tree = torch.zeros_like(self.h_tree, device=dev)
         n = max_nodes
         m = 2 * n * self.W  # mask first so its int64 view stays 8-byte aligned
@@ -58,11 +60,13 @@ class VerifyRunner:
         self.token = self.d_tree[m:m + n]
         self.parent = self.d_tree[m + n:m + 2 * n]
         self.depth = self.d_tree[m + 2 * n:m + 3 * n]
+        self.prefix_dev = self.d_tree[m + 3 * n:m + 3 * n + 1]
         h = self.h_tree.numpy()
         self._h_mask = h[0:m].view(np.uint64).reshape(n, self.W)
         self._h_token = h[m:m + n]
         self._h_parent = h[m + n:m + 2 * n]
         self._h_depth = h[m + 2 * n:m + 3 * n]
+        self._h_hdr = h[m + 3 * n:m + 3 * n + 4]
         self.out = torch.empty(n_layers, max_nodes, n_q_heads, head_dim, dtype=dtype, device=dev)
         self.ids = torch.empty(max_nodes, dtype=torch.int32, device=dev)
         self.max_logit = torch.empty(max_nodes, dtype=torch.float32, device=dev)
@@ -99,6 +103,11 @@ class VerifyRunner:
                            "n_nodes": k, "n_truncated": trunc, "mask_words": self.W}
         return self.packed
 
+    def set_prefix(self, prefix_len: int) -> None:
+        """Stage the prefix length that the next upload carries to
+        ``prefix_dev`` (for steps that read it on the device)."""
+        self._h_hdr[0] = prefix_len
+
     def ensure_workspace(self, prefix_len: int, n_nodes: Optional[int] = None) -> None:
         """Grow the attention workspace (outside any timed or captured region)."""
         n = self.n_nodes if n_nodes is None else n_nodes
@@ -110,10 +119,10 @@ class VerifyRunner:
     def upload_tree(self, stream=None) -> None:
         self.d_tree.copy_(self.h_tree, non_blocking=True)
 
-    def attention(self, layer: int, q, k_layer, v_layer, prefix_len: int, stream=None) -> None:
+    def attention(self, layer: int, q, k_layer, v_layer, prefix_len: int, stream=None, prefix_dev=None) -> None:
         N = self.n_nodes
         ooo.tree_attn(q, k_layer, v_layer, prefix_len, N, self.mask[:N], self.Hq, self.Hkv, self.scale,
-                      self.out[layer, :N], self.attn_ws, stream)
+                      self.out[layer, :N], self.attn_ws, stream, prefix_dev=prefix_dev)
 
     def lm_head(self, hidden, logits=None, stream=None) -> None:
         N = self.n_nodes
@@ -124,8 +133,9 @@ class VerifyRunner:
         ooo.accept(self.token[:N], self.parent[:N], self.depth[:N], self.mask[:N], self.ids[:N], N, self.path,
                    self.accept_len, self.bonus, stream)
 
-    def compact(self, k_cache, v_cache, prefix_len: int, stream=None) -> None:
-        ooo.kv_compact(k_cache, v_cache, prefix_len, self.n_nodes, self.path, self.accept_len, stream)
+    def compact(self, k_cache, v_cache, prefix_len: int, stream=None, prefix_dev=None) -> None:
+        ooo.kv_compact(k_cache, v_cache, prefix_len, self.n_nodes, self.path, self.accept_len, stream,
+                       prefix_dev=prefix_dev)
 
     def download(self) -> None:
         self.h_res.copy_(self.res, non_blocking=True)
@@ -144,13 +154,15 @@ class VerifyRunner:
         self._weight = ooo.lmhead_pack(weight) if packed else weight
 
     def device_step(self, q_layers: Sequence, k_cache, v_cache, hidden, prefix_len: int,
-                    logits=None, compact: bool = True) -> None:
-        """Everything after packing, enqueued on the current stream."""
+                    logits=None, compact: bool = True, prefix_dev=None) -> None:
+        """Everything after packing, enqueued on the current stream.  With
+        ``prefix_dev`` the kernels read P from the device (``prefix_len``
+        bounds it)."""
         self.upload_tree()
         for l in range(self.L_m):
-            self.attention(l, q_layers[l], k_cache[l], v_cache[l], prefix_len)
+            self.attention(l, q_layers[l], k_cache[l], v_cache[l], prefix_len, prefix_dev=prefix_dev)
         self.lm_head(hidden, logits)
         self.accept()
         if compact:
-            self.compact(k_cache, v_cache, prefix_len)
+            self.compact(k_cache, v_cache, prefix_len, prefix_dev=prefix_dev)
         self.download()

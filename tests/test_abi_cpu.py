@@ -172,8 +172,8 @@ def test_layer_entry_points_validate_on_host():
 
     def qk(**kw):
         a = {**args, **kw}
-        return L.ooo_qk_norm_rope(a["qkv"], a["qn"], a["kn"], a["eps"], a["depth"], a["N"], a["P"], a["theta"],
-                                  a["Hq"], a["Hkv"], a["D"], a["q"], a["kc"], a["vc"], a["cap"], None)
+        return L.ooo_qk_norm_rope(a["qkv"], a["qn"], a["kn"], a["eps"], a["depth"], a["N"], a["P"], None,
+                                  a["theta"], a["Hq"], a["Hkv"], a["D"], a["q"], a["kc"], a["vc"], a["cap"], None)
     assert qk(qkv=None) == ooo.ERR_INVALID
     assert qk(depth=None) == ooo.ERR_INVALID
     assert qk(P=97) == ooo.ERR_INVALID  # P + N > cap
@@ -188,33 +188,33 @@ def test_device_entry_points_validate_on_host():
     L = ooo.lib()
     fake = ctypes.c_void_p(256)  # never dereferenced: every call below fails validation first
     # null pointers
-    assert L.ooo_tree_attn(None, fake, fake, 100, 10, 4, fake, 1, 4, 1, 64, 0.1, ooo.BF16, fake, None, 0, None) \
+    assert L.ooo_tree_attn(None, fake, fake, 100, 10, None, 4, fake, 1, 4, 1, 64, 0.1, ooo.BF16, fake, None, 0, None) \
         == ooo.ERR_INVALID
     assert "null" in ooo.last_error()
     assert L.ooo_lmhead_argmax(fake, None, 4, 64, 100, ooo.BF16, ooo.W_ROWS, fake, fake, None, fake, 1 << 20, None) \
         == ooo.ERR_INVALID
     assert L.ooo_accept(fake, fake, fake, fake, 1, fake, 4, 8, None, fake, fake, None) == ooo.ERR_INVALID
-    assert L.ooo_kv_compact(fake, fake, 2, 2, 100, 64, ooo.BF16, 10, 4, None, fake, 8, None) == ooo.ERR_INVALID
+    assert L.ooo_kv_compact(fake, fake, 2, 2, 100, 64, ooo.BF16, 10, None, 4, None, fake, 8, None) == ooo.ERR_INVALID
     # inconsistent shapes
-    assert L.ooo_tree_attn(fake, fake, fake, 100, 97, 4, fake, 1, 4, 1, 64, 0.1, ooo.BF16, fake, None, 0, None) \
+    assert L.ooo_tree_attn(fake, fake, fake, 100, 97, None, 4, fake, 1, 4, 1, 64, 0.1, ooo.BF16, fake, None, 0, None) \
         == ooo.ERR_INVALID  # P + N > cap
-    assert L.ooo_tree_attn(fake, fake, fake, 100, 10, 4, fake, 1, 6, 4, 64, 0.1, ooo.BF16, fake, None, 0, None) \
+    assert L.ooo_tree_attn(fake, fake, fake, 100, 10, None, 4, fake, 1, 6, 4, 64, 0.1, ooo.BF16, fake, None, 0, None) \
         == ooo.ERR_INVALID  # Hq % Hkv
-    assert L.ooo_tree_attn(fake, fake, fake, 100, 10, 65, fake, 1, 4, 1, 64, 0.1, ooo.BF16, fake, None, 0, None) \
+    assert L.ooo_tree_attn(fake, fake, fake, 100, 10, None, 65, fake, 1, 4, 1, 64, 0.1, ooo.BF16, fake, None, 0, None) \
         == ooo.ERR_INVALID  # too few mask words
-    assert L.ooo_tree_attn(fake, fake, fake, 100, 10, 0, fake, 1, 4, 1, 64, 0.1, ooo.BF16, fake, None, 0, None) \
+    assert L.ooo_tree_attn(fake, fake, fake, 100, 10, None, 0, fake, 1, 4, 1, 64, 0.1, ooo.BF16, fake, None, 0, None) \
         == ooo.ERR_INVALID
     assert L.ooo_accept(fake, fake, fake, fake, 1, fake, 65, 8, fake, fake, fake, None) == ooo.ERR_INVALID
     assert L.ooo_accept(fake, fake, fake, fake, 1, fake, 4, 0, fake, fake, fake, None) == ooo.ERR_INVALID
-    assert L.ooo_kv_compact(fake, fake, 2, 2, 100, 64, ooo.BF16, 97, 4, fake, fake, 8, None) == ooo.ERR_INVALID
+    assert L.ooo_kv_compact(fake, fake, 2, 2, 100, 64, ooo.BF16, 97, None, 4, fake, fake, 8, None) == ooo.ERR_INVALID
     # unsupported but valid
-    assert L.ooo_tree_attn(fake, fake, fake, 100, 10, 4, fake, 1, 4, 1, 96, 0.1, ooo.BF16, fake, None, 0, None) \
+    assert L.ooo_tree_attn(fake, fake, fake, 100, 10, None, 4, fake, 1, 4, 1, 96, 0.1, ooo.BF16, fake, None, 0, None) \
         == ooo.ERR_UNSUPPORTED
     assert L.ooo_lmhead_argmax(fake, fake, 4, 100, 1000, ooo.BF16, ooo.W_ROWS, fake, fake, None, fake, 1 << 20, None) \
         == ooo.ERR_UNSUPPORTED
     assert L.ooo_lmhead_argmax(fake, fake, 300, 128, 1000, ooo.BF16, ooo.W_ROWS, fake, fake, None, fake, 1 << 20, None) \
         == ooo.ERR_UNSUPPORTED
-    assert L.ooo_kv_compact(fake, fake, 2, 2, 100, 4, ooo.BF16, 10, 4, fake, fake, 8, None) == ooo.ERR_UNSUPPORTED
+    assert L.ooo_kv_compact(fake, fake, 2, 2, 100, 4, ooo.BF16, 10, None, 4, fake, fake, 8, None) == ooo.ERR_UNSUPPORTED
     # weight layouts
     assert L.ooo_lmhead_argmax(fake, fake, 4, 64, 1000, ooo.BF16, 2, fake, fake, None, fake, 1 << 20, None) \
         == ooo.ERR_INVALID
@@ -234,6 +234,6 @@ def test_device_entry_points_validate_on_host():
         == ooo.ERR_CAPACITY
     need = L.ooo_tree_attn_workspace(64, 32, 8, 128, 4096, ooo.BF16)
     assert need > 0
-    assert L.ooo_tree_attn(fake, fake, fake, 4160, 4096, 64, fake, 1, 32, 8, 128, 0.1, ooo.BF16, fake, fake,
+    assert L.ooo_tree_attn(fake, fake, fake, 4160, 4096, None, 64, fake, 1, 32, 8, 128, 0.1, ooo.BF16, fake, fake,
                            need - 1, None) == ooo.ERR_CAPACITY
     assert ooo.last_error() != ""

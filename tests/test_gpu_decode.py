@@ -1,0 +1,295 @@
+"""Decoding rounds on the GPU against the CPU reference, through the C ABI.
+
+* The prefix length read from device memory (``prefix_dev``, what a replayed
+  graph uses while the prefix grows) gives the results of the same call with
+  that prefix length passed directly: bitwise for the rotation/cache writes
+  and the compaction, within tolerance of the reference for the attention
+  (its split plan follows the bound), including splits left empty by a
+  device prefix far below the bound.
+* ``DecodeLoop`` (readiness check at the candidate boundary, Eq. 3; Merge_B;
+  verify and commit, Section 4.5) on a 2-layer model: per round the same
+  hint readiness, lanes, trie size, accepted length, bonus token and
+  committed tokens as ``oracle/decode_loop.py``, with graph replay, with
+  eager launches (bitwise the same caches) and with a hint delivered by a
+  real thread at an unpredictable round.  Integers are compared exactly on
+  rounds whose reference margins at the accepted path are at least 2e-2
+  (asserted, so a seed with a near tie fails loudly instead of passing).
+"""
+
+from __future__ import annotations
+
+import concurrent.futures
+import dataclasses
+import math
+import time
+
+import numpy as np
+import pytest
+import torch
+
+import gpu_harness as gh
+from oracle import decode_loop as odl
+from oracle import target_model as om
+from oracle import tree_verify as ov
+from paper_2608_00814_amd import model_workload as mw
+from paper_2608_00814_amd import ooo
+from paper_2608_00814_amd import workload as wl
+from paper_2608_00814_amd.decode import DecodeLoop, SidecarHint
+from paper_2608_00814_amd.model import ModelRunner
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+TOL = gh.ATTN_TOL
+f64 = wl.bf16_to_f64
+MARGIN = 2e-2
+
+
+def _prefix_dev(P):
+    return torch.tensor([P], dtype=torch.int32, device=DEV)
+
+
+# ----------------------------------------------------------------------------
+# kernels with the prefix length in device memory
+
+
+@pytest.mark.parametrize("P,bound,N,Hq,Hkv", [(4096, 4096, 64, 32, 8), (1000, 4096, 64, 32, 8),
+                                              (10, 4096, 64, 32, 8), (0, 3000, 5, 8, 2), (77, 200, 33, 4, 1)])
+def test_attention_device_prefix(P, bound, N, Hq, Hkv):
+    print(f"case attention device prefix P={P} bound={bound} N={N} Hq={Hq} Hkv={Hkv}", flush=True)
+    D = 128
+    rs = np.random.default_rng(P + bound + N)
+    cap = bound + N
+    parent = np.array([-1] + [int(rs.integers(0, i)) for i in range(1, N)], np.int32)
+    W = (N + 63) // 64
+    mask = ov.ancestor_masks(parent, W)
+    q = wl.to_bf16_bits(rs.normal(size=(N, Hq, D)).astype(np.float32))
+    k = wl.to_bf16_bits(rs.normal(size=(Hkv, cap, D)).astype(np.float32))
+    v = wl.to_bf16_bits(rs.normal(size=(Hkv, cap, D)).astype(np.float32))
+    qd, kd, vd = (gh.to_dev(a, "bf16", DEV) for a in (q, k, v))
+    # node rows sit at P + i for the device prefix; the rows between the
+    # device prefix and the bound are ordinary cache rows nobody reads
+    md = torch.from_numpy(mask.view(np.int64)).to(DEV).view(N, W)
+    scale = 1.0 / math.sqrt(D)
+    ws = torch.zeros(ooo.tree_attn_workspace(N, Hq, Hkv, D, bound, ooo.BF16) // 4 + 1, device=DEV)
+    ws2 = torch.zeros(ooo.tree_attn_workspace(N, Hq, Hkv, D, P, ooo.BF16) // 4 + 1, device=DEV)
+    out_dev = torch.empty(N, Hq, D, dtype=torch.bfloat16, device=DEV)
+    out_host = torch.empty_like(out_dev)
+    ooo.tree_attn(qd, kd, vd, bound, N, md, Hq, Hkv, scale, out_dev, ws, prefix_dev=_prefix_dev(P))
+    ooo.tree_attn(qd, kd, vd, P, N, md, Hq, Hkv, scale, out_host, ws2)
+    torch.cuda.synchronize()
+    if P == bound:
+        assert torch.equal(out_dev, out_host)
+    ref = ov.tree_attention(f64(q), f64(k), f64(v), P, parent, Hkv)
+    got = f64(gh.to_host(out_dev, "bf16"))
+    assert gh.row_rel_err(got.reshape(N * Hq, D), ref.reshape(N * Hq, D)) <= TOL
+
+
+def test_rotation_and_compaction_device_prefix():
+    print("case qk_norm_rope and kv_compact with a device prefix", flush=True)
+    rs = np.random.default_rng(9)
+    N, Hq, Hkv, D, P, bound = 24, 8, 2, 128, 333, 900
+    cap = bound + N
+    qkv = wl.to_bf16_bits(rs.normal(size=(N, (Hq + 2 * Hkv) * D)).astype(np.float32))
+    qn = wl.to_bf16_bits(1.0 + 0.2 * rs.normal(size=D).astype(np.float32))
+    kn = wl.to_bf16_bits(1.0 + 0.2 * rs.normal(size=D).astype(np.float32))
+    depth = torch.from_numpy(rs.integers(0, 20, size=N).astype(np.int32)).to(DEV)
+    args = (gh.to_dev(qkv, "bf16", DEV), gh.to_dev(qn, "bf16", DEV), gh.to_dev(kn, "bf16", DEV), 1e-6, depth, N)
+    outs = []
+    for via_dev in (True, False):
+        kc = torch.full((2, Hkv, cap, D), 1.0, dtype=torch.bfloat16, device=DEV)
+        vc = torch.full_like(kc, 2.0)
+        q_out = torch.empty(N, Hq, D, dtype=torch.bfloat16, device=DEV)
+        for l in range(2):
+            if via_dev:
+                ooo.qk_norm_rope(*args, bound, 1e6, Hq, Hkv, q_out, kc[l], vc[l], prefix_dev=_prefix_dev(P))
+            else:
+                ooo.qk_norm_rope(*args, P, 1e6, Hq, Hkv, q_out, kc[l], vc[l])
+        path = torch.tensor([0, 3, 9, 10, 17], dtype=torch.int32, device=DEV)
+        L = torch.tensor([4], dtype=torch.int32, device=DEV)
+        if via_dev:
+            ooo.kv_compact(kc, vc, bound, N, path, L, prefix_dev=_prefix_dev(P))
+        else:
+            ooo.kv_compact(kc, vc, P, N, path, L)
+        torch.cuda.synchronize()
+        outs.append((q_out.clone(), kc.clone(), vc.clone()))
+    for a, b in zip(outs[0], outs[1]):
+        assert torch.equal(a, b)
+    # rows outside [P, P + N) untouched
+    kc = outs[0][1]
+    assert (kc[:, :, :P] == 1.0).all() and (kc[:, :, P + N:] == 1.0).all()
+
+
+# ----------------------------------------------------------------------------
+# the decode loop
+
+
+class _ChecksUntilReady:
+    """A future that reports done from its (n + 1)-th done() call on."""
+
+    def __init__(self, views, n):
+        self.views, self.n, self.calls, self.results = views, n, 0, 0
+
+    def done(self):
+        self.calls += 1
+        return self.calls > self.n
+
+    def result(self):
+        self.results += 1
+        return self.views
+
+
+@dataclasses.dataclass
+class _Case:
+    cfg: mw.ModelConfig
+    lws: list
+    emb: np.ndarray
+    fin: np.ndarray
+    lm: np.ndarray
+    ref_layers: list
+    shp: om.ModelShape
+    kv: list
+    root: int
+    native: object
+    views: list
+
+
+def _native(cfg, seed):
+    def fn(r, committed):
+        g = np.random.default_rng([seed, r, 11])
+        return [[int(t) for t in g.integers(0, cfg.vocab - 1, size=4)],
+                [int(t) for t in g.integers(0, cfg.vocab - 1, size=3)]]
+    return fn
+
+
+def _ref_caches(case):
+    cfg = case.cfg
+    kcs, vcs = [], []
+    for k, v in case.kv:
+        kc = np.zeros((cfg.n_kv_heads, cfg.cap, cfg.head_dim))
+        vc = np.zeros_like(kc)
+        kc[:, :k.shape[1]] = f64(k)
+        vc[:, :v.shape[1]] = f64(v)
+        kcs.append(kc)
+        vcs.append(vc)
+    return kcs, vcs
+
+
+class _Widen:
+    def __init__(self, bits):
+        self.bits = bits
+        self.shape = bits.shape
+
+    def __getitem__(self, idx):
+        return f64(self.bits[idx])
+
+
+def _oracle(case, rounds, views, done):
+    cfg = case.cfg
+    kcs, vcs = _ref_caches(case)
+    return odl.run_rounds(rounds, cfg.prefix_len, case.root, case.native, views, done, lambda r, y: True,
+                          cfg.vocab - 1, 6, 7, cfg.max_nodes, cfg.max_depth, _Widen(case.emb), case.ref_layers,
+                          f64(case.fin), _Widen(case.lm), case.shp, kcs, vcs)
+
+
+def _case(seed, rounds_greedy=24):
+    cfg = dataclasses.replace(mw.MODEL_CONFIGS["small-model"], cap=260)
+    lws = [mw.layer_weights(cfg, seed, l) for l in range(cfg.n_layers)]
+    emb, fin, lm = mw.embedding(cfg, seed), mw.final_norm(cfg, seed), mw.lm_head(cfg, seed)
+    ref_layers = [om.LayerWeights(**{k: f64(v) for k, v in lw.items()}) for lw in lws]
+    shp = om.ModelShape(hidden=cfg.hidden, n_q_heads=cfg.n_q_heads, n_kv_heads=cfg.n_kv_heads,
+                        head_dim=cfg.head_dim, intermediate=cfg.intermediate, rope_theta=cfg.rope_theta,
+                        eps=cfg.eps)
+    kv = [mw.prefix_kv(cfg, seed, l) for l in range(cfg.n_layers)]
+    root = mw.random_tokens(cfg, seed, 1)[0]
+    case = _Case(cfg, lws, emb, fin, lm, ref_layers, shp, kv, root, _native(cfg, seed), [])
+    # the target's own continuation (native candidates only), for the hint view
+    plain = _oracle(case, rounds_greedy, None, lambda r: False)
+    greedy = plain["committed"][1:]
+    rs = np.random.default_rng(seed)
+    decoy = [int(t) for t in rs.integers(0, cfg.vocab - 1, size=40)]
+    case.views = [decoy, [case.root] + greedy[:40]]
+    return case
+
+
+def _check_margins(ref):
+    for rec in ref["records"]:
+        m = rec["margin"][rec["path"]]
+        assert m.min() >= MARGIN, f"round {rec['round']}: reference margin {m.min():.2e} at the accepted path"
+
+
+def _gpu_loop(case, hint, rounds, graphs):
+    cfg = case.cfg
+    runner = ModelRunner(cfg, case.lws, case.emb, case.fin, case.lm, DEV)
+    kc = torch.zeros(cfg.n_layers, cfg.n_kv_heads, cfg.cap, cfg.head_dim, dtype=torch.bfloat16, device=DEV)
+    vc = torch.zeros_like(kc)
+    for l, (k, v) in enumerate(case.kv):
+        kc[l, :, :k.shape[1]] = gh.to_dev(k, "bf16", DEV)
+        vc[l, :, :v.shape[1]] = gh.to_dev(v, "bf16", DEV)
+    torch.cuda.synchronize()
+    loop = DecodeLoop(runner, kc, vc, cfg.prefix_len, case.root, case.native, hint=hint, n_lanes=6, max_suffix=7,
+                      graphs=graphs)
+    recs = loop.run(rounds)
+    torch.cuda.synchronize()
+    return loop, recs, kc, vc
+
+
+def _compare(recs, ref):
+    assert len(recs) == len(ref["records"])
+    for g, r in zip(recs, ref["records"]):
+        where = f"round {r['round']}"
+        assert g.prefix_len == r["prefix_len"], where
+        assert g.hint_ready == r["hint_ready"] and g.n_hint == r["n_hint"], where
+        assert g.suffix_len == r["suffix_len"], where
+        assert g.n_nodes == r["n_nodes"], where
+        assert (g.L, g.bonus) == (r["L"], r["bonus"]), (where, g.L, r["L"], g.bonus, r["bonus"])
+        assert g.committed == r["committed"], where
+
+
+SEED = 83
+ROUNDS = 8
+READY_AT = 3
+
+
+def test_decode_loop_graphs_match_reference():
+    """Graph replay (one graph per trie size, prefix from device memory) and
+    eager launches: the reference's rounds, and bitwise-equal caches."""
+    print(f"case decode loop small-model seed={SEED} rounds={ROUNDS} hint ready at round {READY_AT}", flush=True)
+    case = _case(SEED)
+    ref = _oracle(case, ROUNDS, case.views, lambda r: r >= READY_AT)
+    _check_margins(ref)
+    assert any(rec["n_hint"] for rec in ref["records"]) and max(rec["L"] for rec in ref["records"]) >= 4
+    fut = _ChecksUntilReady(case.views, READY_AT)
+    loop, recs, kc, vc = _gpu_loop(case, SidecarHint(fut, case.cfg.vocab - 1), ROUNDS, graphs=True)
+    assert loop.hint.first_ready_round == READY_AT and fut.results == 1  # the bank is built once
+    _compare(recs, ref)
+    assert loop.committed == ref["committed"]
+    fut2 = _ChecksUntilReady(case.views, READY_AT)
+    _, recs2, kc2, vc2 = _gpu_loop(case, SidecarHint(fut2, case.cfg.vocab - 1), ROUNDS, graphs=False)
+    _compare(recs2, ref)
+    P = ref["prefix_len"]
+    assert torch.equal(kc[:, :, :P], kc2[:, :, :P]) and torch.equal(vc[:, :, :P], vc2[:, :, :P])
+    # committed cache rows against the reference's (bf16 rounding of fp64 rows)
+    kcs, vcs = _ref_caches(case)
+    odl.run_rounds(ROUNDS, case.cfg.prefix_len, case.root, case.native, case.views, lambda r: r >= READY_AT,
+                   lambda r, y: True, case.cfg.vocab - 1, 6, 7, case.cfg.max_nodes, case.cfg.max_depth,
+                   _Widen(case.emb), case.ref_layers, f64(case.fin), _Widen(case.lm), case.shp, kcs, vcs)
+    for l in range(case.cfg.n_layers):
+        assert gh.row_rel_err(f64(gh.to_host(kc[l], "bf16")[:, :P]), kcs[l][:, :P]) <= TOL
+        assert gh.row_rel_err(f64(gh.to_host(vc[l], "bf16")[:, :P]), vcs[l][:, :P]) <= TOL
+
+
+def test_decode_loop_threaded_hint():
+    """The hint comes from a real thread that finishes at an unpredictable
+    moment; whatever round first sees it, the rounds equal the reference's
+    rounds with the readiness observed at that round."""
+    print(f"case decode loop small-model seed={SEED} threaded hint", flush=True)
+    case = _case(SEED)
+    with concurrent.futures.ThreadPoolExecutor(max_workers=1) as ex:
+        fut = ex.submit(lambda: (time.sleep(0.05), case.views)[1])
+        loop, recs, _, _ = _gpu_loop(case, SidecarHint(fut, case.cfg.vocab - 1), ROUNDS, graphs=True)
+    s = loop.hint.first_ready_round
+    ready = (lambda r: False) if s is None else (lambda r: r >= s)
+    ref = _oracle(case, ROUNDS, case.views, ready)
+    _check_margins(ref)
+    _compare(recs, ref)
+    print(f"  hint first seen at round {s}", flush=True)
