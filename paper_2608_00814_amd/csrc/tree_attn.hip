@@ -9,6 +9,10 @@
 //  * Work item = (KV head g, block of 32*WAVES rows, split s of the key
 //    tiles).  Key tiles are 64 rows: the prefix tiles first, then the tree
 //    tiles [P, P+N) where the ancestor bitmask is tested in registers.
+//    A split is a fixed-length run of tiles, so the key ranges a row's
+//    partial sums cover (and its rounding) do not depend on how many rows
+//    share the launch: for a given key layout a node's output is bitwise
+//    the same in tries of any size.
 //  * Scores are computed transposed, S^T = K Q^T, and the output as
 //    O^T = V^T P^T.  With the A-operand rows of K permuted (bits 2 and 3 of
 //    the row index swapped) every lane ends up holding one query row: its
@@ -55,6 +59,7 @@ struct AttnArgs {
   uint32_t* part_o;  // fp16 normalised partial outputs (fragment order)
   float* part_ml;    // per partial row: max, sum, scale, unused
   int splits, row_blocks, Mpad, tiles_prefix, tiles_total;
+  int tps;           // key tiles per split (split s takes tiles [s tps, (s + 1) tps))
   const int* P_dev;  // null, or the prefix length in device memory (P bounds it)
 };
 
@@ -187,10 +192,12 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
   const int P = a.P_dev ? __builtin_amdgcn_readfirstlane(min(max(*a.P_dev, 0), a.P)) : a.P;
   const int tiles_prefix = (P + kTile - 1) / kTile;
   const int tiles_total = tiles_prefix + (a.N + kTile - 1) / kTile;
-  const int t_begin = (int)((long long)s * tiles_total / a.splits);
-  const int t_end = (int)((long long)(s + 1) * tiles_total / a.splits);
-  // >= 1 when the plan's prefix is the actual one (splits <= tiles); a
-  // shorter device prefix can leave a split empty (handled below)
+  // Fixed runs of tiles: a row's key ranges, and so its rounding, are the
+  // same whatever the trie size and the row block.  >= 1 tile when the
+  // plan's prefix is the actual one; a shorter device prefix can leave
+  // splits empty (handled below).
+  const int t_begin = s * a.tps;
+  const int t_end = min(t_begin + a.tps, tiles_total);
   const int ntiles = t_end - t_begin;
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -817,7 +824,7 @@ __global__ __launch_bounds__(64) void tree_attn_f32_kernel(const float* q, const
 }
 
 struct Plan {
-  int waves, row_blocks, Mpad, tiles_prefix, tiles_total, splits;
+  int waves, row_blocks, Mpad, tiles_prefix, tiles_total, splits, tps;
   size_t ws_bytes;
 };
 
@@ -846,9 +853,11 @@ Plan make_plan(int N, int Hq, int Hkv, int D, int P, ooo_dtype dt) {
   if (splits > 32) splits = 32;
   if (splits > p.tiles_total) splits = p.tiles_total;
   if (splits < 1) splits = 1;
-  p.splits = splits;
-  if (splits > 1)
-    p.ws_bytes = (size_t)splits * Hkv * p.Mpad * (size_t)D * 2 + (size_t)splits * Hkv * p.Mpad * 16 + 256;
+  // fixed-size runs of tiles; the last run may be shorter
+  p.tps = (p.tiles_total + splits - 1) / splits;
+  p.splits = (p.tiles_total + p.tps - 1) / p.tps;
+  if (p.splits > 1)
+    p.ws_bytes = (size_t)p.splits * Hkv * p.Mpad * (size_t)D * 2 + (size_t)p.splits * Hkv * p.Mpad * 16 + 256;
   return p;
 }
 
@@ -923,6 +932,7 @@ extern "C" int ooo_tree_attn(const void* q, const void* k_cache, const void* v_c
     a.Mpad = p.Mpad;
     a.tiles_prefix = p.tiles_prefix;
     a.tiles_total = p.tiles_total;
+    a.tps = p.tps;
     if (p.splits > 1) {
       a.part_o = (uint32_t*)workspace;
       a.part_ml = (float*)((uint8_t*)workspace + (size_t)p.splits * n_kv_heads * p.Mpad * head_dim * 2);
