@@ -44,6 +44,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = 2500.0  # dense bf16 matrix cores
+FP32_PEAK_TFLOPS = 157.3   # fp32 (the tiny fp32 workload runs on the vector units)
 METRIC = "verify steps/s + tree-attn/LM-head HBM GB/s, Qwen3-8B shape, 64-node trie, 4k ctx"
 
 
@@ -744,6 +746,11 @@ def main():
     lm_b = lmhead_bytes(cfg, N)
     lm_gbs = lm_b / (lm_us * 1e-6) / 1e9
     path_gbs = (cfg.n_layers * a_bytes + lm_b) / ((attn_us + lm_us) * 1e-6) / 1e9
+    # attention flops over the prefix keys (4 Hq N P D: scores and P V)
+    a_flops = 4.0 * cfg.n_q_heads * N * P * cfg.head_dim
+    a_tflops = a_flops / (attn_call_us * 1e-6) / 1e12
+    mfma_peak = MFMA_PEAK_TFLOPS if cfg.dtype == "bf16" else FP32_PEAK_TFLOPS
+    mfma_bound = a_flops / a_bytes > mfma_peak * 1e12 / (HBM_PEAK_GBS * 1e9)
 
     out = {
         "metric": METRIC,
@@ -771,11 +778,18 @@ def main():
         "lmhead_us": round(lm_us, 2),
         "path_hbm_gbs": round(path_gbs, 1),
         "path_hbm_frac": round(path_gbs / HBM_PEAK_GBS, 4),
-        "roofline": {"bound": "hbm", "kernel": "ooo_tree_attn (tree_attn_bf16_kernel + tree_attn_combine_kernel)",
-                     "achieved": round(a_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(a_gbs / HBM_PEAK_GBS, 4), "traffic": recorded_traffic(cfg.name, "ooo_tree_attn"),
-                     "bytes_per_launch": a_bytes,
-                     "us_per_launch": round(attn_call_us, 3)},
+        "roofline": ({"bound": "mfma", "kernel": "ooo_tree_attn (tree_attn_bf16_kernel + tree_attn_combine_kernel)",
+                      "achieved": round(a_tflops, 1), "peak": mfma_peak, "unit": "TFLOP/s",
+                      "frac": round(a_tflops / mfma_peak, 4), "traffic": recorded_traffic(cfg.name, "ooo_tree_attn"),
+                      "flops_per_launch": a_flops, "bytes_per_launch": a_bytes,
+                      "us_per_launch": round(attn_call_us, 3)} if mfma_bound else
+                     {"bound": "hbm", "kernel": "ooo_tree_attn (tree_attn_bf16_kernel + tree_attn_combine_kernel)",
+                      "achieved": round(a_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                      "frac": round(a_gbs / HBM_PEAK_GBS, 4), "traffic": recorded_traffic(cfg.name, "ooo_tree_attn"),
+                      "bytes_per_launch": a_bytes,
+                      "us_per_launch": round(attn_call_us, 3)}),
+        "attention_hbm_frac": round(a_gbs / HBM_PEAK_GBS, 4),
+        "attention_mfma_frac": round(a_tflops / mfma_peak, 4),
         "roofline_lmhead": {"bound": "hbm", "kernel": "ooo_lmhead_argmax (lmhead_bf16_kernel + lmhead_finalize_kernel)",
                             "achieved": round(lm_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                             "frac": round(lm_gbs / HBM_PEAK_GBS, 4),

@@ -785,42 +785,85 @@ __global__ __launch_bounds__(256) void tree_attn_combine_kernel(AttnArgs a) {
   }
 }
 
-// float32 path: one wave per (node, query head), keys walked in order with
-// an online softmax; each lane owns head_dim/64 columns.
+// float32 path: one workgroup of 256 threads per (node, query head).  Keys
+// go in chunks of 256, one key per thread: key j is cache row j (prefix
+// rows, then node rows P + i, allowed when bit i of the node's ancestor mask
+// is set).  Each thread scores its key against the query (in LDS), the
+// block takes the chunk's max, and the probabilities go to LDS; then thread
+// t accumulates column t % D of P V over the keys j = t / D (mod 256 / D),
+// with the running max/sum of an online softmax across chunks.  The
+// 256 / D column partials are added at the end.
 template <int D>
-__global__ __launch_bounds__(64) void tree_attn_f32_kernel(const float* q, const float* k, const float* v,
-                                                           long long cap, int P, const int* P_dev, int N,
-                                                           const uint64_t* mask, int W, int Hq, int Hkv, float scale,
-                                                           float* out) {
-  constexpr int C = D / 64;
+__global__ __launch_bounds__(256) void tree_attn_f32_kernel(const float* q, const float* k, const float* v,
+                                                            long long cap, int P, const int* P_dev, int N,
+                                                            const uint64_t* mask, int W, int Hq, int Hkv,
+                                                            float scale, float* out) {
+  constexpr int NT = 256, PARTS = NT / D;
+  __shared__ float qs[D];
+  __shared__ float ps[NT];
+  __shared__ float red[NT / 64];
+  __shared__ float opart[NT];
   if (P_dev) P = min(max(*P_dev, 0), P);
   const int node = blockIdx.x / Hq, head = blockIdx.x % Hq;
   const int g = head / (Hq / Hkv);
-  const int lane = threadIdx.x;
-  float qv[C], o[C];
-  for (int i = 0; i < C; ++i) {
-    qv[i] = q[((size_t)node * Hq + head) * D + lane + 64 * i];
-    o[i] = 0.f;
-  }
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const float sl2 = scale * 1.4426950408889634f;
+  if (t < D) qs[t] = q[((size_t)node * Hq + head) * D + t] * sl2;
   const float* kb = k + (size_t)g * cap * D;
   const float* vb = v + (size_t)g * cap * D;
-  float m = -INFINITY, l = 0.f;
-  auto visit = [&](int rowi) {
-    float part = 0.f;
-    for (int i = 0; i < C; ++i) part += qv[i] * kb[(size_t)rowi * D + lane + 64 * i];
-    for (int off = 32; off > 0; off >>= 1) part += shfl_xor_f(part, off);
-    const float sc = part * scale;
-    const float m_new = fmaxf(m, sc);
-    const float alpha = expf(m - m_new);
-    const float p = expf(sc - m_new);
-    l = l * alpha + p;
-    for (int i = 0; i < C; ++i) o[i] = o[i] * alpha + p * vb[(size_t)rowi * D + lane + 64 * i];
-    m = m_new;
-  };
-  for (int j = 0; j < P; ++j) visit(j);
-  for (int j = 0; j < N; ++j)
-    if ((mask[(size_t)node * W + j / 64] >> (j % 64)) & 1ull) visit(P + j);
-  for (int i = 0; i < C; ++i) out[((size_t)node * Hq + head) * D + lane + 64 * i] = o[i] / l;
+  const uint64_t* mrow = mask + (size_t)node * W;
+  const int col = t % D, part = t / D;
+  float m_run = -INFINITY, l_run = 0.f, o = 0.f;
+  __syncthreads();
+  for (int c0 = 0; c0 < P + N; c0 += NT) {
+    const int j = c0 + t;
+    bool ok = j < P;
+    if (!ok && j < P + N) ok = (mrow[(j - P) >> 6] >> ((j - P) & 63)) & 1ull;
+    float sc = -INFINITY;
+    if (ok) {
+      const float4* kr = reinterpret_cast<const float4*>(kb + (size_t)j * D);
+      float a0 = 0.f, a1 = 0.f;
+#pragma unroll
+      for (int d4 = 0; d4 < D / 4; d4 += 2) {
+        const float4 x = kr[d4], y = kr[d4 + 1];
+        a0 += x.x * qs[4 * d4] + x.y * qs[4 * d4 + 1] + x.z * qs[4 * d4 + 2] + x.w * qs[4 * d4 + 3];
+        a1 += y.x * qs[4 * d4 + 4] + y.y * qs[4 * d4 + 5] + y.z * qs[4 * d4 + 6] + y.w * qs[4 * d4 + 7];
+      }
+      sc = a0 + a1;
+    }
+    float mx = sc;
+    for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, shfl_xor_f(mx, off));
+    if (lane == 0) red[wave] = mx;
+    __syncthreads();
+    mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    const float m_new = fmaxf(m_run, mx);  // finite: every node sees itself
+    const float alpha = exp2f(m_run - m_new);
+    const float p = ok ? exp2f(sc - m_new) : 0.f;
+    ps[t] = p;
+    float sum = p;
+    for (int off = 32; off > 0; off >>= 1) sum += shfl_xor_f(sum, off);
+    __syncthreads();  // ps complete; every wave has read red
+    if (lane == 0) red[wave] = sum;
+    __syncthreads();
+    l_run = l_run * alpha + ((red[0] + red[1]) + (red[2] + red[3]));
+    m_run = m_new;
+    float acc = 0.f;
+    const int nk = min(NT, P + N - c0);
+    for (int jj = part; jj < nk; jj += PARTS) {
+      const float pj = ps[jj];
+      if (pj != 0.f) acc += pj * vb[(size_t)(c0 + jj) * D + col];  // rows of keys not allowed are not read
+    }
+    o = o * alpha + acc;
+    __syncthreads();  // before the next chunk overwrites ps and red
+  }
+  opart[t] = o;
+  __syncthreads();
+  if (t < D) {
+    float s = 0.f;
+#pragma unroll
+    for (int pp = 0; pp < PARTS; ++pp) s += opart[pp * D + t];
+    out[((size_t)node * Hq + head) * D + t] = s / l_run;
+  }
 }
 
 struct Plan {
@@ -900,11 +943,11 @@ extern "C" int ooo_tree_attn(const void* q, const void* k_cache, const void* v_c
   if (dt == OOO_F32) {
     const dim3 grid(n_nodes * n_q_heads);
     if (head_dim == 64)
-      tree_attn_f32_kernel<64><<<grid, 64, 0, st>>>((const float*)q, (const float*)k_cache, (const float*)v_cache,
+      tree_attn_f32_kernel<64><<<grid, 256, 0, st>>>((const float*)q, (const float*)k_cache, (const float*)v_cache,
                                                     cap, prefix_len, prefix_len_dev, n_nodes, anc_mask, mask_words,
                                                     n_q_heads, n_kv_heads, scale, (float*)out);
     else
-      tree_attn_f32_kernel<128><<<grid, 64, 0, st>>>((const float*)q, (const float*)k_cache, (const float*)v_cache,
+      tree_attn_f32_kernel<128><<<grid, 256, 0, st>>>((const float*)q, (const float*)k_cache, (const float*)v_cache,
                                                      cap, prefix_len, prefix_len_dev, n_nodes, anc_mask,
                                                      mask_words, n_q_heads, n_kv_heads, scale, (float*)out);
   } else {

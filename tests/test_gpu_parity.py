@@ -108,6 +108,8 @@ ATTN_CASES = [
     (128, 25, 4, 1, 64, "random", "f32"),
     (1, 40, 2, 2, 128, "deep", "f32"),
     (0, 3, 1, 1, 64, "star", "f32"),
+    (3000, 70, 4, 2, 128, "random", "f32"),
+    (255, 2, 2, 1, 64, "chain", "f32"),
 ]
 
 
@@ -212,20 +214,21 @@ def test_attention_workspace_reuse_across_shapes(monkeypatch):
         assert gh.row_rel_err(got, ref) <= gh.ATTN_TOL
 
 
-def test_attention_ignores_rows_outside_prefix_and_tree():
-    """Cache rows at and beyond P + N (and non-ancestor tree rows) hold NaN;
-    the output must not see them."""
-    print("case attention NaN rows", flush=True)
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_attention_ignores_rows_outside_prefix_and_tree(dt):
+    """Cache rows at and beyond P + N hold NaN; the output must not see
+    them."""
+    print(f"case attention NaN rows {dt}", flush=True)
     P, N, G, Hkv, D = 100, 20, 4, 2, 128
-    rs, q, k, v, cap = _attn_inputs(P, N, G, Hkv, D, "bf16", seed=11, pad=70)
-    nan = np.uint16(0x7FC0)
+    rs, q, k, v, cap = _attn_inputs(P, N, G, Hkv, D, dt, seed=11, pad=300)
+    nan = np.uint16(0x7FC0) if dt == "bf16" else np.float32("nan")
     k[:, P + N:] = nan
     v[:, P + N:] = nan
     t = _trie("chain", N, rs)
     mask = ov.ancestor_masks(t["parent"], 1)
-    got = _run_attn(q, k, v, P, N, mask, G * Hkv, Hkv, D, "bf16")
+    got = _run_attn(q, k, v, P, N, mask, G * Hkv, Hkv, D, dt)
     assert np.isfinite(got).all()
-    ref = ov.tree_attention(wl.to_f64(q, "bf16"), wl.to_f64(k, "bf16"), wl.to_f64(v, "bf16"), P, t["parent"], Hkv)
+    ref = ov.tree_attention(wl.to_f64(q, dt), wl.to_f64(k, dt), wl.to_f64(v, dt), P, t["parent"], Hkv)
     assert gh.row_rel_err(got, ref) <= gh.ATTN_TOL
 
 
