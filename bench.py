@@ -311,32 +311,33 @@ def bench_model(args):
             vr.upload_tree()
             N = vr.n_nodes
             ooo.embed_rows(runner.emb, vr.token, N, runner.h)
+            ev[0].record(stream)
+            ooo.rmsnorm(runner.h, runner.layers[0]["in_norm"], cfg.eps, runner.x, n_rows=N)
+            ev[1].record(stream)
+            stream.synchronize()
+            phase["other_us"] += 1e3 * ev[0].elapsed_time(ev[1])
             for l, w in enumerate(runner.layers):
+                # the runner's fused calls: projections include their fused
+                # epilogues (norms, rotation and cache writes, residual adds)
                 ev[0].record(stream)
-                ooo.rmsnorm(runner.h, w["in_norm"], cfg.eps, runner.x, n_rows=N)
+                ooo.linear_qk_norm_rope(runner.x, w["w_qkv"], w["q_norm"], w["k_norm"], cfg.eps, vr.depth, N, P,
+                                        cfg.rope_theta, cfg.n_q_heads, cfg.n_kv_heads, runner.q, k_cache[l],
+                                        v_cache[l], runner.lin_ws)
                 ev[1].record(stream)
-                ooo.linear(runner.x, w["w_qkv"], runner.qkv, ooo.EPI_STORE_BF16, runner.lin_ws, n_rows=N)
-                ev[2].record(stream)
-                ooo.qk_norm_rope(runner.qkv, w["q_norm"], w["k_norm"], cfg.eps, vr.depth, N, P, cfg.rope_theta,
-                                 cfg.n_q_heads, cfg.n_kv_heads, runner.q, k_cache[l], v_cache[l])
                 vr.attention(l, runner.q, k_cache[l], v_cache[l], P)
-                ev[3].record(stream)
-                stream.synchronize()
-                phase["other_us"] += 1e3 * ev[0].elapsed_time(ev[1])
-                phase["projections_us"] += 1e3 * ev[1].elapsed_time(ev[2])
-                phase["attention_us"] += 1e3 * ev[2].elapsed_time(ev[3])  # includes the q/k norms and rotation
-                o = vr.out[l].view(cfg.max_nodes, cfg.n_q_heads * cfg.head_dim)
-                ev[0].record(stream)
-                ooo.linear(o, w["w_o"], runner.h, ooo.EPI_ADD_F32, runner.lin_ws, n_rows=N)
-                ev[1].record(stream)
-                ooo.rmsnorm(runner.h, w["post_norm"], cfg.eps, runner.x, n_rows=N)
                 ev[2].record(stream)
+                o = vr.out[l].view(cfg.max_nodes, cfg.n_q_heads * cfg.head_dim)
+                ooo.linear_add_rmsnorm(o, w["w_o"], runner.h, w["post_norm"], cfg.eps, runner.x, runner.lin_ws,
+                                       n_rows=N)
                 ooo.linear(runner.x, w["w_gu"], runner.act, ooo.EPI_SWIGLU_BF16, runner.lin_ws, n_rows=N)
-                ooo.linear(runner.act, w["w_down"], runner.h, ooo.EPI_ADD_F32, runner.lin_ws, n_rows=N)
+                last = l + 1 == len(runner.layers)
+                ooo.linear_add_rmsnorm(runner.act, w["w_down"], runner.h,
+                                       runner.final_norm if last else runner.layers[l + 1]["in_norm"], cfg.eps,
+                                       runner.xf if last else runner.x, runner.lin_ws, n_rows=N)
                 ev[3].record(stream)
                 stream.synchronize()
                 phase["projections_us"] += 1e3 * (ev[0].elapsed_time(ev[1]) + ev[2].elapsed_time(ev[3]))
-                phase["other_us"] += 1e3 * ev[1].elapsed_time(ev[2])
+                phase["attention_us"] += 1e3 * ev[1].elapsed_time(ev[2])
         phase = {k: round(v / reps, 1) for k, v in phase.items()}
 
         Ls = []
@@ -381,7 +382,8 @@ def bench_model(args):
         "tokens_per_s": round(float(np.sum(np.array(Ls) + 1)) / elapsed, 1),
         "mean_accepted_plus_bonus": round(float(np.mean(np.array(Ls) + 1)), 3),
         "phase_us_eager": phase,
-        "roofline": {"bound": "hbm", "kernel": "projections (ooo_linear: qkv, o, gate+up, down over all layers; stream + reduce kernels)",
+        "roofline": {"bound": "hbm", "kernel": ("projections over all layers (qkv with norms/rotation, o_proj and down with residual add + "
+                                "RMSNorm, gate+up with SwiGLU; streaming + epilogue kernels)"),
                      "achieved": round(proj_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(proj_gbs / HBM_PEAK_GBS, 4), "traffic": None, "bytes_per_launch": w_bytes,
                      "us_per_launch": phase["projections_us"]},

@@ -27,6 +27,10 @@
  *   ooo_qk_norm_rope   per-head q/k norms, rotation at position P + depth,
  *                      q out, node k/v into the layer's cache rows
  *   ooo_swiglu         silu(gate) * up of the fused MLP projection
+ *   ooo_linear_add_rmsnorm   a projection added into the residual rows,
+ *                      fused with the RMSNorm that follows it
+ *   ooo_linear_qk_norm_rope  the q/k/v projection fused with the q/k norms,
+ *                      the rotation and the cache writes
  *
  * Conventions shared by every entry point
  *   - Return value: OOO_OK (0) or a negative ooo_status.  On error nothing has
@@ -352,6 +356,53 @@ int ooo_linear_pack(const void* weight, int32_t out_dim, int32_t in_dim, void* p
 int ooo_linear(const void* x, const void* weight, int32_t n_rows, int32_t in_dim, int32_t out_dim,
                int32_t weight_layout, ooo_epilogue epilogue, void* out, void* workspace, size_t ws_bytes,
                void* stream);
+
+/*
+ * ooo_linear_add_rmsnorm - a projection whose output is added into the
+ * residual rows, fused with the RMSNorm that follows it in the target's
+ * layer (o_proj then the post-attention norm; down then the next layer's
+ * input norm or the final norm; Section 4.5: one forward pass over the tree).
+ *
+ * DEVICE pointers; asynchronous on `stream`.
+ *   x, weight, n_rows, in_dim, out_dim, weight_layout, workspace, ws_bytes
+ *                as for ooo_linear (workspace sized by ooo_linear_workspace)
+ *   residual     [n_rows][out_dim] float32, updated in place:
+ *                residual += x weight^T
+ *   norm_weight  [out_dim] bf16
+ *   normed_out   [n_rows][out_dim] bf16:
+ *                residual / sqrt(mean(residual^2) + eps) * norm_weight
+ * The partial sums are added in the same order as ooo_linear's
+ * OOO_EPI_ADD_F32, so `residual` matches that epilogue bitwise.
+ * Errors: those of ooo_linear; OOO_ERR_INVALID (null residual, norm_weight
+ * or normed_out, eps < 0); OOO_ERR_UNSUPPORTED (out_dim % 4 != 0 or
+ * out_dim > 8192).
+ */
+int ooo_linear_add_rmsnorm(const void* x, const void* weight, int32_t n_rows, int32_t in_dim, int32_t out_dim,
+                           int32_t weight_layout, float* residual, const void* norm_weight, float eps,
+                           void* normed_out, void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * ooo_linear_qk_norm_rope - the fused q/k/v projection of the trie's rows
+ * followed by what ooo_qk_norm_rope does with it (per-head norms of q and
+ * k, rotation at position P + depth[i], q to q_out, k and v to cache row
+ * P + i; Section 4.5), computed from the projection's float32 sums (no bf16
+ * rounding in between).
+ *
+ * DEVICE pointers; asynchronous on `stream`.
+ *   x, weight, n_rows, in_dim, weight_layout, workspace, ws_bytes   as for
+ *                ooo_linear, with out_dim = (n_q_heads + 2 n_kv_heads)
+ *                head_dim (q rows, then k rows, then v rows)
+ *   the rest as for ooo_qk_norm_rope (n_rows trie nodes; prefix_len_dev
+ *   NULL or the device prefix length that prefix_len bounds)
+ * Errors: those of ooo_linear and ooo_qk_norm_rope; OOO_ERR_UNSUPPORTED when
+ * (n_q_heads + 2 n_kv_heads) head_dim is not a multiple of 128.
+ */
+int ooo_linear_qk_norm_rope(const void* x, const void* weight, int32_t n_rows, int32_t in_dim,
+                            int32_t weight_layout, const void* q_norm, const void* k_norm, float eps,
+                            const int32_t* depth, int32_t prefix_len, const int32_t* prefix_len_dev,
+                            double rope_theta, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                            void* q_out, void* k_cache, void* v_cache, int64_t cap, void* workspace,
+                            size_t ws_bytes, void* stream);
 
 /*
  * ooo_qk_norm_rope - queries of the trie nodes and their keys/values in the

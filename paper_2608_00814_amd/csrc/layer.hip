@@ -16,13 +16,10 @@
 
 #include "device_common.h"
 #include "ooo_internal.h"
+#include "rope.h"
 
 namespace ooo {
 namespace {
-
-__device__ __forceinline__ uint16_t f32_to_bf16_bits(float v) {
-  return (uint16_t)(pack_bf16x2(v, 0.f) & 0xFFFFu);
-}
 
 // ---------------------------------------------------------------- embedding
 // One block per node, 16-byte loads (8 bf16); a token outside [0, V)
@@ -101,11 +98,6 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
 // precision and reduced by multiples of 2 pi before a float sine/cosine.  Heads [0, Hq) are queries, [Hq, Hq + Hkv) keys,
 // [Hq + Hkv, Hq + 2 Hkv) values (copied to the cache unchanged).  A null norm
 // weight skips that norm (models without QK norms).
-// Rotation frequencies theta^(-2j/D), computed on the host in double.
-struct RopeFreq {
-  double f[64];
-};
-
 template <int D>
 __global__ __launch_bounds__(1024) void qk_norm_rope_kernel(const uint16_t* __restrict__ qkv,
                                                            const uint16_t* __restrict__ q_norm,
@@ -125,14 +117,7 @@ __global__ __launch_bounds__(1024) void qk_norm_rope_kernel(const uint16_t* __re
   const long long row = (long long)P + n;  // node n's cache row
   const bool act = lane < HALF;
   float cs = 1.f, sn = 0.f;
-  if (act) {
-    // angle in double, reduced by multiples of 2 pi (two-term constant), so
-    // a float sine/cosine of a small argument finishes it
-    const double ang = (double)(P + depth[n]) * fr.f[lane];
-    const double k = rint(ang * 0.15915494309189535);
-    const double red = fma(-k, 2.4492935982947064e-16, fma(-k, 6.283185307179586, ang));
-    sincosf((float)red, &sn, &cs);
-  }
+  if (act) rope_sincos(P + depth[n], fr.f[lane], sn, cs);
   {
     const uint16_t* hr = src + (size_t)hh * D;
     if (hh >= Hq + Hkv) {
@@ -147,21 +132,11 @@ __global__ __launch_bounds__(1024) void qk_norm_rope_kernel(const uint16_t* __re
     const bool is_q = hh < Hq;
     float a = act ? bf16_bits_to_f32(hr[lane]) : 0.f;
     float b = act ? bf16_bits_to_f32(hr[lane + HALF]) : 0.f;
-    const uint16_t* nw = is_q ? q_norm : k_norm;
-    if (nw) {
-      float ss = __builtin_fmaf(a, a, b * b);
-      for (int off = 32; off > 0; off >>= 1) ss += shfl_xor_f(ss, off);
-      const float r = 1.f / sqrtf(ss / (float)D + eps);
-      if (act) {
-        a = a * r * bf16_bits_to_f32(nw[lane]);
-        b = b * r * bf16_bits_to_f32(nw[lane + HALF]);
-      }
-    }
-    const float ra = a * cs - b * sn, rb = b * cs + a * sn;
+    norm_rotate(a, b, act, is_q ? q_norm : k_norm, eps, D, lane, cs, sn);
     uint16_t* dst = is_q ? q_out + ((size_t)n * Hq + hh) * D : k_cache + ((size_t)(hh - Hq) * cap + row) * D;
     if (act) {
-      dst[lane] = f32_to_bf16_bits(ra);
-      dst[lane + HALF] = f32_to_bf16_bits(rb);
+      dst[lane] = f32_to_bf16_bits(a);
+      dst[lane + HALF] = f32_to_bf16_bits(b);
     }
   }
 }
@@ -225,8 +200,7 @@ extern "C" int ooo_qk_norm_rope(const void* qkv, const void* q_norm, const void*
   OOO_REQUIRE(head_dim == 64 || head_dim == 128, OOO_ERR_UNSUPPORTED,
               "ooo_qk_norm_rope: head_dim %d not supported (64 or 128)", head_dim);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  RopeFreq fr{};
-  for (int j = 0; j < head_dim / 2; ++j) fr.f[j] = pow(rope_theta, -2.0 * j / head_dim);
+  const RopeFreq fr = rope_freq(rope_theta, head_dim);
   const dim3 grid(n_nodes, (n_q_heads + 2 * n_kv_heads + 15) / 16);
   if (head_dim == 128)
     qk_norm_rope_kernel<128><<<grid, 1024, 0, st>>>((const uint16_t*)qkv, (const uint16_t*)q_norm,

@@ -22,8 +22,11 @@
 //    rows), or silu(gate) * up of a fused gate/up projection.
 #include <math.h>
 
+#include <vector>
+
 #include "device_common.h"
 #include "ooo_internal.h"
+#include "rope.h"
 
 namespace ooo {
 namespace {
@@ -257,6 +260,141 @@ __global__ __launch_bounds__(256) void linear_reduce_kernel(const float* __restr
   }
 }
 
+// Sum of the partials at element e (node n, tile row r: e = n * 128 + r)
+// over a tile's slot list (from tile_slots), in block order as the reduce
+// kernel adds them (same rounding); loads issued four at a time.
+template <typename T>
+__device__ __forceinline__ T slot_sum_of(const float* __restrict__ part, const int* slots, int ns, size_t stride,
+                                         size_t e) {
+  T s{};
+  int i = 0;
+  for (; i + 4 <= ns; i += 4) {
+    const T x0 = *reinterpret_cast<const T*>(part + slots[i] * stride + e);
+    const T x1 = *reinterpret_cast<const T*>(part + slots[i + 1] * stride + e);
+    const T x2 = *reinterpret_cast<const T*>(part + slots[i + 2] * stride + e);
+    const T x3 = *reinterpret_cast<const T*>(part + slots[i + 3] * stride + e);
+    s += x0;
+    s += x1;
+    s += x2;
+    s += x3;
+  }
+  for (; i < ns; ++i) s += *reinterpret_cast<const T*>(part + slots[i] * stride + e);
+  return s;
+}
+
+// Slot-list capacity of the fused epilogues (checked on the host).
+constexpr int kMaxTileSlots = 64;
+constexpr int kMaxFusedTiles = 64;
+
+// Projection epilogue fused with the next RMSNorm: for row n,
+// h[n] += the projection (its partial sums), then out[n] = bf16(h[n] /
+// sqrt(mean(h[n]^2) + eps) * w).  One block of 512 threads per row, four
+// float4 columns per thread (out_dim <= 8192).
+constexpr int kAddNormItems = 4;
+__global__ __launch_bounds__(512) void linear_add_rmsnorm_kernel(const float* __restrict__ part, int npad, int K,
+                                                                 int O, int B, int seg, float* __restrict__ resid,
+                                                                 const uint16_t* __restrict__ w, float eps,
+                                                                 uint16_t* __restrict__ out) {
+  __shared__ float red[8];
+  __shared__ int slots[kMaxFusedTiles][kMaxTileSlots];
+  __shared__ int nslots[kMaxFusedTiles];
+  const int n = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int KC = K / 64;
+  const int tiles = (O + kRows - 1) / kRows;
+  const long long C = (long long)tiles * KC;
+  if ((int)threadIdx.x < tiles) nslots[threadIdx.x] = tile_slots(C, B, KC, seg, threadIdx.x, slots[threadIdx.x]);
+  __syncthreads();
+  const size_t stride = (size_t)npad * kRows;
+  float* hrow = resid + (size_t)n * O;
+  f32x4 hv[kAddNormItems];
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < kAddNormItems; ++i) {
+    const int c = 4 * (threadIdx.x + 512 * i);
+    hv[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (c < O) {
+      const int t = c / kRows;
+      const f32x4 sv = slot_sum_of<f32x4>(part, slots[t], nslots[t], stride, (size_t)n * kRows + c % kRows);
+      hv[i] = *reinterpret_cast<const f32x4*>(hrow + c) + sv;
+      *reinterpret_cast<f32x4*>(hrow + c) = hv[i];
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < kAddNormItems; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) ss = __builtin_fmaf(hv[i][e], hv[i][e], ss);
+  for (int off = 32; off > 0; off >>= 1) ss += shfl_xor_f(ss, off);
+  if (lane == 0) red[wave] = ss;
+  __syncthreads();
+  const float tot = ((red[0] + red[1]) + (red[2] + red[3])) + ((red[4] + red[5]) + (red[6] + red[7]));
+  const float r = 1.f / sqrtf(tot / (float)O + eps);
+#pragma unroll
+  for (int i = 0; i < kAddNormItems; ++i) {
+    const int c = 4 * (threadIdx.x + 512 * i);
+    if (c < O) {
+      const u32x2 wv = *reinterpret_cast<const u32x2*>(w + c);
+      u32x2 o;
+      o[0] = pack_bf16x2(hv[i][0] * r * __uint_as_float(wv[0] << 16), hv[i][1] * r * __uint_as_float(wv[0] & 0xFFFF0000u));
+      o[1] = pack_bf16x2(hv[i][2] * r * __uint_as_float(wv[1] << 16), hv[i][3] * r * __uint_as_float(wv[1] & 0xFFFF0000u));
+      *reinterpret_cast<u32x2*>(out + (size_t)n * O + c) = o;
+    }
+  }
+}
+
+// Projection epilogue fused with the q/k norms and the rotation: block
+// (node n, 16 heads), one wave per head of the fused q/k/v projection.  Lane
+// j < D/2 sums the partials of its pair (j, j + D/2) in float32 and then
+// proceeds as the rotation kernel: per-head RMSNorm of q and k, rotation at
+// position P + depth[n], q to q_out, k and v (rounded to bf16) to cache row
+// P + n.
+template <int D>
+__global__ __launch_bounds__(1024) void linear_qk_norm_rope_kernel(
+    const float* __restrict__ part, int npad, int K, int B, int seg, const uint16_t* __restrict__ q_norm,
+    const uint16_t* __restrict__ k_norm, float eps, const int32_t* __restrict__ depth, int P,
+    const int32_t* __restrict__ P_dev, RopeFreq fr, int Hq, int Hkv, uint16_t* __restrict__ q_out,
+    uint16_t* __restrict__ k_cache, uint16_t* __restrict__ v_cache, long long cap) {
+  constexpr int HALF = D / 2;
+  static_assert(kRows % D == 0, "a head lies in one tile");
+  if (P_dev) P = min(max(*P_dev, 0), P);
+  const int n = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int nh = Hq + 2 * Hkv;
+  const int hh = blockIdx.y * 16 + wave;
+  if (hh >= nh) return;
+  __shared__ int slots[16][kMaxTileSlots];
+  __shared__ int nslots[16];
+  const int KC = K / 64;
+  const long long C = (long long)(nh * D / kRows) * KC;
+  const size_t stride = (size_t)npad * kRows;
+  const int t = hh * D / kRows, r0 = hh * D % kRows;
+  if (lane == 0) nslots[wave] = tile_slots(C, B, KC, seg, t, slots[wave]);
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  const long long row = (long long)P + n;
+  const bool act = lane < HALF;
+  float a = 0.f, b = 0.f;
+  if (act) {
+    a = slot_sum_of<float>(part, slots[wave], nslots[wave], stride, (size_t)n * kRows + r0 + lane);
+    b = slot_sum_of<float>(part, slots[wave], nslots[wave], stride, (size_t)n * kRows + r0 + lane + HALF);
+  }
+  if (hh >= Hq + Hkv) {
+    uint16_t* dst = v_cache + ((size_t)(hh - Hq - Hkv) * cap + row) * D;
+    if (act) {
+      dst[lane] = f32_to_bf16_bits(a);
+      dst[lane + HALF] = f32_to_bf16_bits(b);
+    }
+    return;
+  }
+  float cs = 1.f, sn = 0.f;
+  if (act) rope_sincos(P + depth[n], fr.f[lane], sn, cs);
+  const bool is_q = hh < Hq;
+  norm_rotate(a, b, act, is_q ? q_norm : k_norm, eps, D, lane, cs, sn);
+  uint16_t* dst = is_q ? q_out + ((size_t)n * Hq + hh) * D : k_cache + ((size_t)(hh - Hq) * cap + row) * D;
+  if (act) {
+    dst[lane] = f32_to_bf16_bits(a);
+    dst[lane + HALF] = f32_to_bf16_bits(b);
+  }
+}
+
 struct LinPlan {
   int nb, blocks, seg;
   size_t ws_bytes;
@@ -293,23 +431,37 @@ extern "C" size_t ooo_linear_workspace(int32_t n_rows, int32_t in_dim, int32_t o
   return lin_plan(n_rows, in_dim, out_dim).ws_bytes;
 }
 
-extern "C" int ooo_linear(const void* x, const void* weight, int32_t n_rows, int32_t in_dim, int32_t out_dim,
-                          int32_t weight_layout, ooo_epilogue epilogue, void* out, void* workspace, size_t ws_bytes,
-                          void* stream) {
-  OOO_REQUIRE(x && weight && out, OOO_ERR_INVALID, "ooo_linear: null pointer");
-  OOO_REQUIRE(n_rows >= 1 && in_dim >= 1 && out_dim >= 1, OOO_ERR_INVALID, "ooo_linear: sizes must be positive");
-  OOO_REQUIRE(weight_layout == OOO_W_ROWS || weight_layout == OOO_W_PACKED, OOO_ERR_INVALID,
-              "ooo_linear: unknown weight layout %d", weight_layout);
-  OOO_REQUIRE(epilogue >= OOO_EPI_STORE_F32 && epilogue <= OOO_EPI_SWIGLU_BF16, OOO_ERR_INVALID,
-              "ooo_linear: unknown epilogue %d", (int)epilogue);
-  OOO_REQUIRE(in_dim % 64 == 0, OOO_ERR_UNSUPPORTED, "ooo_linear: in_dim %% 64 != 0");
-  OOO_REQUIRE(n_rows <= 256, OOO_ERR_UNSUPPORTED, "ooo_linear: at most 256 rows");
-  OOO_REQUIRE(epilogue != OOO_EPI_SWIGLU_BF16 || out_dim % 256 == 0, OOO_ERR_UNSUPPORTED,
-              "ooo_linear: the SwiGLU epilogue needs out_dim %% 256 == 0 (gate and up halves of whole tiles)");
+// Largest number of stream-K blocks whose runs meet one output tile (the
+// length of that tile's slot list).
+static int max_tile_slots(int n_rows, int in_dim, int out_dim) {
   const LinPlan p = lin_plan(n_rows, in_dim, out_dim);
-  OOO_REQUIRE(workspace && ws_bytes >= p.ws_bytes, OOO_ERR_CAPACITY,
-              "ooo_linear: workspace of %zu bytes needed (got %zu)", p.ws_bytes, ws_bytes);
-  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const int KC = in_dim / 64, tiles = (out_dim + kRows - 1) / kRows;
+  const long long C = (long long)tiles * KC;
+  std::vector<int> count(tiles, 0);
+  for (int b = 0; b < p.blocks; ++b) {
+    const long long lo = run_lo(C, b, p.blocks), hi = run_lo(C, b + 1, p.blocks);
+    if (hi <= lo) continue;
+    for (long long t = lo / KC; t <= (hi - 1) / KC; ++t) ++count[t];
+  }
+  int m = 0;
+  for (int c : count) m = c > m ? c : m;
+  return m;
+}
+
+// Validation and the streaming kernel shared by the entry points; on
+// success the partial sums are in the workspace and *plan is set.
+static int stream_k(const char* who, const void* x, const void* weight, int32_t n_rows, int32_t in_dim,
+                    int32_t out_dim, int32_t weight_layout, void* workspace, size_t ws_bytes, hipStream_t st,
+                    LinPlan* plan) {
+  OOO_REQUIRE(x && weight, OOO_ERR_INVALID, "%s: null pointer", who);
+  OOO_REQUIRE(n_rows >= 1 && in_dim >= 1 && out_dim >= 1, OOO_ERR_INVALID, "%s: sizes must be positive", who);
+  OOO_REQUIRE(weight_layout == OOO_W_ROWS || weight_layout == OOO_W_PACKED, OOO_ERR_INVALID,
+              "%s: unknown weight layout %d", who, weight_layout);
+  OOO_REQUIRE(in_dim % 64 == 0, OOO_ERR_UNSUPPORTED, "%s: in_dim %% 64 != 0", who);
+  OOO_REQUIRE(n_rows <= 256, OOO_ERR_UNSUPPORTED, "%s: at most 256 rows", who);
+  const LinPlan p = lin_plan(n_rows, in_dim, out_dim);
+  OOO_REQUIRE(workspace && ws_bytes >= p.ws_bytes, OOO_ERR_CAPACITY, "%s: workspace of %zu bytes needed (got %zu)",
+              who, p.ws_bytes, ws_bytes);
   const uint16_t* X = (const uint16_t*)x;
   const uint16_t* W = (const uint16_t*)weight;
   float* part = (float*)workspace;
@@ -326,11 +478,101 @@ extern "C" int ooo_linear(const void* x, const void* weight, int32_t n_rows, int
   else if (p.nb == 4) OOO_LIN_LAUNCH(4);
   else OOO_LIN_LAUNCH(8);
 #undef OOO_LIN_LAUNCH
+  *plan = p;
+  return OOO_OK;
+}
+
+extern "C" int ooo_linear(const void* x, const void* weight, int32_t n_rows, int32_t in_dim, int32_t out_dim,
+                          int32_t weight_layout, ooo_epilogue epilogue, void* out, void* workspace, size_t ws_bytes,
+                          void* stream) {
+  OOO_REQUIRE(out, OOO_ERR_INVALID, "ooo_linear: null pointer");
+  OOO_REQUIRE(epilogue >= OOO_EPI_STORE_F32 && epilogue <= OOO_EPI_SWIGLU_BF16, OOO_ERR_INVALID,
+              "ooo_linear: unknown epilogue %d", (int)epilogue);
+  OOO_REQUIRE(epilogue != OOO_EPI_SWIGLU_BF16 || out_dim % 256 == 0, OOO_ERR_UNSUPPORTED,
+              "ooo_linear: the SwiGLU epilogue needs out_dim %% 256 == 0 (gate and up halves of whole tiles)");
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  LinPlan p{};
+  const int rc = stream_k("ooo_linear", x, weight, n_rows, in_dim, out_dim, weight_layout, workspace, ws_bytes, st, &p);
+  if (rc != OOO_OK) return rc;
+  float* part = (float*)workspace;
   const int tiles = (out_dim + kRows - 1) / kRows;
   const int rgrid = 4 * (epilogue == OOO_EPI_SWIGLU_BF16 ? tiles / 2 : tiles);
   linear_reduce_kernel<<<rgrid, 256, 0, st>>>(part, n_rows, 32 * p.nb, in_dim, out_dim, p.blocks, p.seg, (int)epilogue,
                                               out, out_dim / 2);
   const hipError_t e = hipGetLastError();
   OOO_REQUIRE(e == hipSuccess, OOO_ERR_HIP, "ooo_linear: launch failed: %s", hipGetErrorString(e));
+  return ooo::ok();
+}
+
+extern "C" int ooo_linear_add_rmsnorm(const void* x, const void* weight, int32_t n_rows, int32_t in_dim,
+                                      int32_t out_dim, int32_t weight_layout, float* residual,
+                                      const void* norm_weight, float eps, void* normed_out, void* workspace,
+                                      size_t ws_bytes, void* stream) {
+  OOO_REQUIRE(residual && norm_weight && normed_out, OOO_ERR_INVALID, "ooo_linear_add_rmsnorm: null pointer");
+  OOO_REQUIRE(eps >= 0.f, OOO_ERR_INVALID, "ooo_linear_add_rmsnorm: eps must be >= 0");
+  OOO_REQUIRE(out_dim % 4 == 0 && out_dim <= 512 * 4 * kAddNormItems, OOO_ERR_UNSUPPORTED,
+              "ooo_linear_add_rmsnorm: out_dim %d must be a multiple of 4 and at most %d", out_dim,
+              512 * 4 * kAddNormItems);
+  OOO_REQUIRE(n_rows < 1 || in_dim < 64 || in_dim % 64 || n_rows > 256 ||
+                  max_tile_slots(n_rows, in_dim, out_dim) <= kMaxTileSlots,
+              OOO_ERR_UNSUPPORTED, "ooo_linear_add_rmsnorm: more than %d partial slots per tile at this shape",
+              kMaxTileSlots);
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  LinPlan p{};
+  const int rc = stream_k("ooo_linear_add_rmsnorm", x, weight, n_rows, in_dim, out_dim, weight_layout, workspace,
+                          ws_bytes, st, &p);
+  if (rc != OOO_OK) return rc;
+  linear_add_rmsnorm_kernel<<<n_rows, 512, 0, st>>>((const float*)workspace, 32 * p.nb, in_dim, out_dim, p.blocks,
+                                                     p.seg, residual, (const uint16_t*)norm_weight, eps,
+                                                     (uint16_t*)normed_out);
+  const hipError_t e = hipGetLastError();
+  OOO_REQUIRE(e == hipSuccess, OOO_ERR_HIP, "ooo_linear_add_rmsnorm: launch failed: %s", hipGetErrorString(e));
+  return ooo::ok();
+}
+
+extern "C" int ooo_linear_qk_norm_rope(const void* x, const void* weight, int32_t n_rows, int32_t in_dim,
+                                       int32_t weight_layout, const void* q_norm, const void* k_norm, float eps,
+                                       const int32_t* depth, int32_t prefix_len, const int32_t* prefix_len_dev,
+                                       double rope_theta, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                       void* q_out, void* k_cache, void* v_cache, int64_t cap, void* workspace,
+                                       size_t ws_bytes, void* stream) {
+  OOO_REQUIRE(depth && q_out && k_cache && v_cache, OOO_ERR_INVALID, "ooo_linear_qk_norm_rope: null pointer");
+  OOO_REQUIRE(n_q_heads >= 1 && n_kv_heads >= 1 && prefix_len >= 0, OOO_ERR_INVALID,
+              "ooo_linear_qk_norm_rope: sizes must be positive");
+  OOO_REQUIRE((int64_t)prefix_len + n_rows <= cap, OOO_ERR_INVALID,
+              "ooo_linear_qk_norm_rope: prefix_len + n_rows (%lld) exceeds cap (%lld)", (long long)prefix_len + n_rows,
+              (long long)cap);
+  OOO_REQUIRE(rope_theta > 0.0 && eps >= 0.f, OOO_ERR_INVALID, "ooo_linear_qk_norm_rope: rope_theta must be > 0");
+  OOO_REQUIRE(head_dim == 64 || head_dim == 128, OOO_ERR_UNSUPPORTED,
+              "ooo_linear_qk_norm_rope: head_dim %d not supported (64 or 128)", head_dim);
+  const int nh = n_q_heads + 2 * n_kv_heads;
+  OOO_REQUIRE((int64_t)nh * head_dim % kRows == 0, OOO_ERR_UNSUPPORTED,
+              "ooo_linear_qk_norm_rope: (n_q_heads + 2 n_kv_heads) * head_dim must be a multiple of %d", kRows);
+  OOO_REQUIRE(n_rows < 1 || in_dim < 64 || in_dim % 64 || n_rows > 256 ||
+                  max_tile_slots(n_rows, in_dim, nh * head_dim) <= kMaxTileSlots,
+              OOO_ERR_UNSUPPORTED, "ooo_linear_qk_norm_rope: more than %d partial slots per tile at this shape",
+              kMaxTileSlots);
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  LinPlan p{};
+  const int rc = stream_k("ooo_linear_qk_norm_rope", x, weight, n_rows, in_dim, nh * head_dim, weight_layout,
+                          workspace, ws_bytes, st, &p);
+  if (rc != OOO_OK) return rc;
+  const RopeFreq fr = rope_freq(rope_theta, head_dim);
+  const dim3 grid(n_rows, (nh + 15) / 16);
+  const float* part = (const float*)workspace;
+  if (head_dim == 128)
+    linear_qk_norm_rope_kernel<128><<<grid, 1024, 0, st>>>(part, 32 * p.nb, in_dim, p.blocks, p.seg,
+                                                            (const uint16_t*)q_norm, (const uint16_t*)k_norm, eps, depth,
+                                                            prefix_len, prefix_len_dev, fr, n_q_heads, n_kv_heads,
+                                                            (uint16_t*)q_out, (uint16_t*)k_cache, (uint16_t*)v_cache,
+                                                            cap);
+  else
+    linear_qk_norm_rope_kernel<64><<<grid, 1024, 0, st>>>(part, 32 * p.nb, in_dim, p.blocks, p.seg,
+                                                           (const uint16_t*)q_norm, (const uint16_t*)k_norm, eps, depth,
+                                                           prefix_len, prefix_len_dev, fr, n_q_heads, n_kv_heads,
+                                                           (uint16_t*)q_out, (uint16_t*)k_cache, (uint16_t*)v_cache,
+                                                           cap);
+  const hipError_t e = hipGetLastError();
+  OOO_REQUIRE(e == hipSuccess, OOO_ERR_HIP, "ooo_linear_qk_norm_rope: launch failed: %s", hipGetErrorString(e));
   return ooo::ok();
 }

@@ -17,6 +17,12 @@ compaction):
         h  += a Wd^T                                      ooo_linear (add into h)
     X = rmsnorm(h); greedy tokens; accept; compact        (VerifyRunner)
 
+By default the projections' epilogues are fused into their consumers: the
+qkv projection with the norms, rotation and cache writes
+(ooo_linear_qk_norm_rope), o_proj and down with the residual add and the
+following RMSNorm (ooo_linear_add_rmsnorm); 10 launches per layer instead of
+13.
+
 The residual rows stay in float32; every projection reads bf16 operands and
 accumulates in float32.  Projection weights are packed once, at load, into
 the streaming layout of ooo_linear_pack.
@@ -40,9 +46,13 @@ def _bits_to_dev(a: np.ndarray, dev) -> torch.Tensor:
 
 class ModelRunner:
     def __init__(self, cfg: ModelConfig, layers: Sequence[Dict[str, np.ndarray]], embedding: np.ndarray,
-                 final_norm: np.ndarray, lm_head: np.ndarray, device="cuda"):
-        """Weights as bf16 bit patterns (uint16, ``model_workload`` layout)."""
+                 final_norm: np.ndarray, lm_head: np.ndarray, device="cuda", fused: bool = True):
+        """Weights as bf16 bit patterns (uint16, ``model_workload`` layout).
+        ``fused``: projections with their consumers fused into the epilogue
+        (ooo_linear_qk_norm_rope, ooo_linear_add_rmsnorm); False issues the
+        separate calls."""
         self.cfg = cfg
+        self.fused = fused
         dev = torch.device(device)
         self.device = dev
         self.vr = VerifyRunner(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.hidden, cfg.vocab,
@@ -93,18 +103,37 @@ class ModelRunner:
         vr.ensure_workspace(P)  # allocates only for a larger shape than seen before (never inside a capture)
         ws = self.lin_ws
         ooo.embed_rows(self.emb, vr.token, N, self.h)
+        if not self.fused:
+            for l, w in enumerate(self.layers):
+                ooo.rmsnorm(self.h, w["in_norm"], cfg.eps, self.x, n_rows=N)
+                ooo.linear(self.x, w["w_qkv"], self.qkv, ooo.EPI_STORE_BF16, ws, n_rows=N)
+                ooo.qk_norm_rope(self.qkv, w["q_norm"], w["k_norm"], cfg.eps, vr.depth, N, P, cfg.rope_theta,
+                                 cfg.n_q_heads, cfg.n_kv_heads, self.q, k_cache[l], v_cache[l], prefix_dev=prefix_dev)
+                vr.attention(l, self.q, k_cache[l], v_cache[l], P, prefix_dev=prefix_dev)
+                o = vr.out[l].view(cfg.max_nodes, cfg.n_q_heads * cfg.head_dim)
+                ooo.linear(o, w["w_o"], self.h, ooo.EPI_ADD_F32, ws, n_rows=N)
+                ooo.rmsnorm(self.h, w["post_norm"], cfg.eps, self.x, n_rows=N)
+                ooo.linear(self.x, w["w_gu"], self.act, ooo.EPI_SWIGLU_BF16, ws, n_rows=N)
+                ooo.linear(self.act, w["w_down"], self.h, ooo.EPI_ADD_F32, ws, n_rows=N)
+            ooo.rmsnorm(self.h, self.final_norm, cfg.eps, self.xf, n_rows=N)
+            return
+        # The same layers with the projections' epilogues fused into their
+        # consumers: qkv + norms/rotation/cache writes, o_proj + residual add
+        # + post-attention norm, down + residual add + the next layer's input
+        # norm (the final norm after the last layer).
+        ooo.rmsnorm(self.h, self.layers[0]["in_norm"], cfg.eps, self.x, n_rows=N)
         for l, w in enumerate(self.layers):
-            ooo.rmsnorm(self.h, w["in_norm"], cfg.eps, self.x, n_rows=N)
-            ooo.linear(self.x, w["w_qkv"], self.qkv, ooo.EPI_STORE_BF16, ws, n_rows=N)
-            ooo.qk_norm_rope(self.qkv, w["q_norm"], w["k_norm"], cfg.eps, vr.depth, N, P, cfg.rope_theta,
-                             cfg.n_q_heads, cfg.n_kv_heads, self.q, k_cache[l], v_cache[l], prefix_dev=prefix_dev)
+            ooo.linear_qk_norm_rope(self.x, w["w_qkv"], w["q_norm"], w["k_norm"], cfg.eps, vr.depth, N, P,
+                                    cfg.rope_theta, cfg.n_q_heads, cfg.n_kv_heads, self.q, k_cache[l], v_cache[l],
+                                    ws, prefix_dev=prefix_dev)
             vr.attention(l, self.q, k_cache[l], v_cache[l], P, prefix_dev=prefix_dev)
             o = vr.out[l].view(cfg.max_nodes, cfg.n_q_heads * cfg.head_dim)
-            ooo.linear(o, w["w_o"], self.h, ooo.EPI_ADD_F32, ws, n_rows=N)
-            ooo.rmsnorm(self.h, w["post_norm"], cfg.eps, self.x, n_rows=N)
+            ooo.linear_add_rmsnorm(o, w["w_o"], self.h, w["post_norm"], cfg.eps, self.x, ws, n_rows=N)
             ooo.linear(self.x, w["w_gu"], self.act, ooo.EPI_SWIGLU_BF16, ws, n_rows=N)
-            ooo.linear(self.act, w["w_down"], self.h, ooo.EPI_ADD_F32, ws, n_rows=N)
-        ooo.rmsnorm(self.h, self.final_norm, cfg.eps, self.xf, n_rows=N)
+            last = l + 1 == len(self.layers)
+            nxt = self.final_norm if last else self.layers[l + 1]["in_norm"]
+            ooo.linear_add_rmsnorm(self.act, w["w_down"], self.h, nxt, cfg.eps, self.xf if last else self.x, ws,
+                                   n_rows=N)
 
     def device_step(self, k_cache: torch.Tensor, v_cache: torch.Tensor, prefix_len: int,
                     logits: Optional[torch.Tensor] = None, compact: bool = True, prefix_dev=None) -> None:

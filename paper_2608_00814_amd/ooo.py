@@ -57,6 +57,11 @@ SIGNATURES = {
     "ooo_qk_norm_rope": (ctypes.c_int, [_vp, _vp, _vp, ctypes.c_float, _vp, _i32, _i32, _vp, ctypes.c_double, _i32,
                                         _i32, _i32, _vp, _vp, _vp, _i64, _vp]),
     "ooo_swiglu": (ctypes.c_int, [_vp, _i32, _i32, _vp, _vp]),
+    "ooo_linear_add_rmsnorm": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp, ctypes.c_float, _vp, _vp,
+                                              _sz, _vp]),
+    "ooo_linear_qk_norm_rope": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _vp, _vp, ctypes.c_float, _vp, _i32, _vp,
+                                               ctypes.c_double, _i32, _i32, _i32, _vp, _vp, _vp, _i64, _vp, _sz,
+                                               _vp]),
 }
 
 
@@ -407,6 +412,46 @@ def linear(x, weight, out, epilogue: int, workspace, n_rows: Optional[int] = Non
     ws_bytes = workspace.numel() * workspace.element_size()
     _check(lib().ooo_linear(x.data_ptr(), wptr, n, K, O, layout, int(epilogue), out.data_ptr(), workspace.data_ptr(),
                             ws_bytes, _stream(stream)))
+
+
+def _weight_args(weight):
+    if isinstance(weight, PackedLinear):
+        return weight.data.data_ptr(), W_PACKED, weight.shape
+    _dev(weight, "weight")
+    return weight.data_ptr(), W_ROWS, tuple(weight.shape)
+
+
+def linear_add_rmsnorm(x, weight, residual, norm_weight, eps: float, normed_out, workspace,
+                       n_rows: Optional[int] = None, stream=None) -> None:
+    """residual[:n] += x[:n] @ weight.T (float32 rows, in place), then
+    normed_out[:n] = rmsnorm(residual[:n]) * norm_weight in bf16."""
+    for t, nm in ((x, "x"), (residual, "residual"), (norm_weight, "norm_weight"), (normed_out, "normed_out")):
+        _dev(t, nm)
+    n = x.shape[0] if n_rows is None else n_rows
+    wptr, layout, (O, K) = _weight_args(weight)
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib().ooo_linear_add_rmsnorm(x.data_ptr(), wptr, n, K, O, layout, residual.data_ptr(),
+                                        norm_weight.data_ptr(), float(eps), normed_out.data_ptr(),
+                                        workspace.data_ptr(), ws_bytes, _stream(stream)))
+
+
+def linear_qk_norm_rope(x, weight, q_norm, k_norm, eps: float, depth, n_nodes: int, prefix_len: int,
+                        rope_theta: float, n_q_heads: int, n_kv_heads: int, q_out, k_cache, v_cache, workspace,
+                        stream=None, prefix_dev=None) -> None:
+    """The fused q/k/v projection of x[:n] followed by the q/k norms, the
+    rotation at P + depth and the cache writes (as ``qk_norm_rope`` on the
+    projection's float32 sums)."""
+    for t, nm in ((x, "x"), (depth, "depth"), (q_out, "q_out"), (k_cache, "k_cache"), (v_cache, "v_cache")):
+        _dev(t, nm)
+    wptr, layout, (O, K) = _weight_args(weight)
+    _, cap, D = k_cache.shape
+    if O != (n_q_heads + 2 * n_kv_heads) * D:
+        raise ValueError(f"weight has {O} rows, expected (Hq + 2 Hkv) * D = {(n_q_heads + 2 * n_kv_heads) * D}")
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib().ooo_linear_qk_norm_rope(x.data_ptr(), wptr, n_nodes, K, layout, _ptr(q_norm), _ptr(k_norm),
+                                         float(eps), depth.data_ptr(), prefix_len, _prefix_ptr(prefix_dev),
+                                         float(rope_theta), n_q_heads, n_kv_heads, D, q_out.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), cap,
+                                         workspace.data_ptr(), ws_bytes, _stream(stream)))
 
 
 def qk_norm_rope(qkv, q_norm, k_norm, eps: float, depth, n_nodes: int, prefix_len: int, rope_theta: float,

@@ -27,7 +27,7 @@ def declared_functions():
 
 def test_exports_match_header():
     names = declared_functions()
-    assert len(names) == 20
+    assert len(names) == 22
     assert set(names) == set(ooo.SIGNATURES)
     lib = ooo.lib()
     for n in names:
@@ -182,6 +182,23 @@ def test_layer_entry_points_validate_on_host():
     assert qk(D=96) == ooo.ERR_UNSUPPORTED
     assert L.ooo_swiglu(None, 4, 64, fake, None) == ooo.ERR_INVALID
     assert L.ooo_swiglu(fake, 4, 0, fake, None) == ooo.ERR_INVALID
+    # fused projection epilogues: rejected on the host, nothing enqueued
+    ws_need = ooo.linear_workspace(64, 4096, 4096)
+    assert L.ooo_linear_add_rmsnorm(fake, fake, 64, 4096, 4096, ooo.W_PACKED, None, fake, 1e-6, fake, fake,
+                                    ws_need, None) == ooo.ERR_INVALID
+    assert L.ooo_linear_add_rmsnorm(fake, fake, 64, 4096, 8196, ooo.W_PACKED, fake, fake, 1e-6, fake, fake,
+                                    1 << 30, None) == ooo.ERR_UNSUPPORTED
+    assert L.ooo_linear_add_rmsnorm(fake, fake, 64, 4096, 4096, ooo.W_PACKED, fake, fake, -1.0, fake, fake,
+                                    ws_need, None) == ooo.ERR_INVALID
+    assert L.ooo_linear_add_rmsnorm(fake, fake, 64, 4096, 4096, ooo.W_PACKED, fake, fake, 1e-6, fake, fake,
+                                    ws_need - 1, None) == ooo.ERR_CAPACITY
+    qk = lambda **kw: L.ooo_linear_qk_norm_rope(
+        fake, fake, kw.get("N", 64), 4096, ooo.W_PACKED, fake, fake, 1e-6, kw.get("depth", fake), kw.get("P", 10),
+        None, 1e6, 32, 8, kw.get("D", 128), fake, fake, fake, kw.get("cap", 5000), fake, kw.get("ws", 1 << 30), None)
+    assert qk(depth=None) == ooo.ERR_INVALID
+    assert qk(P=4990) == ooo.ERR_INVALID  # P + N > cap
+    assert qk(D=96) == ooo.ERR_UNSUPPORTED
+    assert qk(ws=16) == ooo.ERR_CAPACITY
 
 
 def test_device_entry_points_validate_on_host():

@@ -89,6 +89,106 @@ def test_linear(N, K, O, packed):
     torch.cuda.synchronize()
 
 
+@pytest.mark.parametrize("N,K,O", [(64, 4096, 4096), (37, 12288, 4096), (1, 256, 256), (5, 512, 1024),
+                                   (64, 1024, 8192)])
+def test_linear_add_rmsnorm(N, K, O):
+    """The projection added into the residual rows and the following RMSNorm
+    in one call: the residual rows bitwise equal to ooo_linear's add
+    epilogue, the normalised rows within tolerance of the reference."""
+    print(f"case linear_add_rmsnorm N={N} K={K} O={O}", flush=True)
+    rs = np.random.default_rng(N + K + O + 1)
+    x, w = _bits(rs, (N, K)), _bits(rs, (O, K), 0.02)
+    nw = wl.to_bf16_bits(1.0 + 0.2 * rs.normal(size=O).astype(np.float32))
+    base = rs.normal(size=(N, O)).astype(np.float32)
+    xd, wp = _dev_bf16(x), ooo.linear_pack(_dev_bf16(w))
+    ws = torch.zeros(ooo.linear_workspace(N, K, O), dtype=torch.uint8, device=DEV)
+    h_fused = torch.from_numpy(base).to(DEV)
+    h_ref = h_fused.clone()
+    out = torch.empty(N, O, dtype=torch.bfloat16, device=DEV)
+    ooo.linear_add_rmsnorm(xd, wp, h_fused, _dev_bf16(nw), 1e-6, out, ws)
+    ooo.linear(xd, wp, h_ref, ooo.EPI_ADD_F32, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(h_fused, h_ref)
+    ref_h = base.astype(np.float64) + f64(x) @ f64(w).T
+    assert gh.row_rel_err(h_fused.double().cpu().numpy(), ref_h) <= 1e-4
+    assert gh.row_rel_err(_host_f64(out), om.rmsnorm(h_fused.double().cpu().numpy(), f64(nw), 1e-6)) <= TOL
+
+
+@pytest.mark.parametrize("N,Hq,Hkv,D,P,bound", [(64, 32, 8, 128, 4096, None), (33, 4, 2, 64, 100, None),
+                                                (1, 8, 2, 128, 0, None), (20, 16, 8, 128, 700, 2000)])
+def test_linear_qk_norm_rope(N, Hq, Hkv, D, P, bound):
+    """The q/k/v projection fused with the norms, the rotation at P + depth
+    and the cache writes, against the reference layer's projection; with a
+    device prefix below the bound when ``bound`` is set."""
+    print(f"case linear_qk_norm_rope N={N} Hq={Hq} Hkv={Hkv} D={D} P={P} bound={bound}", flush=True)
+    rs = np.random.default_rng(N + Hq + D + P + 3)
+    H = 1024
+    O = (Hq + 2 * Hkv) * D
+    x, w = _bits(rs, (N, H)), _bits(rs, (O, H), 0.05)
+    qn = wl.to_bf16_bits(1.0 + 0.2 * rs.normal(size=D).astype(np.float32))
+    kn = wl.to_bf16_bits(1.0 + 0.2 * rs.normal(size=D).astype(np.float32))
+    depth = rs.integers(0, 40, size=N).astype(np.int32)
+    depth[0] = 0
+    theta = 1.0e6
+    cap = (bound if bound is not None else P) + N + 3
+    kc = torch.full((Hkv, cap, D), 1.0, dtype=torch.bfloat16, device=DEV)
+    vc = torch.full((Hkv, cap, D), 1.0, dtype=torch.bfloat16, device=DEV)
+    q_out = torch.empty(N, Hq, D, dtype=torch.bfloat16, device=DEV)
+    ws = torch.zeros(ooo.linear_workspace(N, H, O), dtype=torch.uint8, device=DEV)
+    pdev = None if bound is None else torch.tensor([P], dtype=torch.int32, device=DEV)
+    ooo.linear_qk_norm_rope(_dev_bf16(x), ooo.linear_pack(_dev_bf16(w)), _dev_bf16(qn), _dev_bf16(kn), 1e-6,
+                            torch.from_numpy(depth).to(DEV), N, P if bound is None else bound, theta, Hq, Hkv,
+                            q_out, kc, vc, ws, prefix_dev=pdev)
+    torch.cuda.synchronize()
+    lw = om.LayerWeights(in_norm=None, w_qkv=f64(w), q_norm=f64(qn), k_norm=f64(kn), w_o=None, post_norm=None,
+                         w_gate=None, w_up=None, w_down=None)
+    shp = om.ModelShape(hidden=H, n_q_heads=Hq, n_kv_heads=Hkv, head_dim=D, intermediate=0, rope_theta=theta)
+    q_ref, k_ref, v_ref = om.project_qkv(f64(x), lw, shp, P + depth.astype(np.int64))
+    assert gh.row_rel_err(_host_f64(q_out).reshape(N * Hq, D), q_ref.reshape(N * Hq, D)) <= TOL
+    kh, vh = gh.to_host(kc, "bf16"), gh.to_host(vc, "bf16")
+    assert gh.row_rel_err(f64(kh[:, P:P + N].transpose(1, 0, 2)).reshape(-1, D), k_ref.reshape(-1, D)) <= TOL
+    assert gh.row_rel_err(f64(vh[:, P:P + N].transpose(1, 0, 2)).reshape(-1, D), v_ref.reshape(-1, D)) <= TOL
+    sentinel = np.uint16(0x3F80)
+    for arr in (kh, vh):
+        assert (arr[:, :P] == sentinel).all() and (arr[:, P + N:] == sentinel).all()
+
+
+def test_model_fused_matches_separate_calls():
+    """The decoder with fused projection epilogues against the same decoder
+    issued as separate calls: LM-head input rows within tolerance, equal
+    greedy tokens where the reference margin allows, and the same accepted
+    path."""
+    print("case model fused vs separate calls (qwen3-8b-model, 2 layers)", flush=True)
+    import dataclasses
+    cfg = dataclasses.replace(mw.MODEL_CONFIGS["qwen3-8b-model"], n_layers=2)
+    seed = 4
+    lws, emb, fin, lm, _, _ = _model(cfg, seed, cfg.n_layers)
+    kv = [mw.prefix_kv(cfg, seed, l) for l in range(cfg.n_layers)]
+    toks = mw.random_tokens(cfg, seed, 80)
+    cands = [toks[1:41], toks[41:53], toks[1:5] + toks[53:63], toks[63:75]]
+    offs = np.zeros(len(cands) + 1, np.int32)
+    offs[1:] = np.cumsum([len(c) for c in cands])
+    flat = np.array([t for c in cands for t in c], np.int32)
+    outs = []
+    for fused in (True, False):
+        runner = ModelRunner(cfg, lws, emb, fin, lm, DEV, fused=fused)
+        kc = torch.stack([_dev_bf16(k) for k, _ in kv])
+        vc = torch.stack([_dev_bf16(v) for _, v in kv])
+        runner.pack(toks[0], flat, offs)
+        logits = torch.empty(runner.vr.n_nodes, cfg.vocab, dtype=torch.float32, device=DEV)
+        runner.device_step(kc, vc, cfg.prefix_len, logits=logits)
+        torch.cuda.synchronize()
+        outs.append((_host_f64(runner.xf[:runner.vr.n_nodes]), logits.cpu().numpy(), runner.result()))
+        del runner, kc, vc
+    (xa, la, ra), (xb, lb, rb) = outs
+    assert gh.row_rel_err(xa, xb) <= TOL
+    top = np.sort(lb, axis=1)
+    safe = (top[:, -1] - top[:, -2]) >= 1e-2
+    assert np.array_equal(la.argmax(1)[safe], lb.argmax(1)[safe])
+    if safe[rb.path].all():
+        assert ra.L == rb.L and np.array_equal(ra.path, rb.path) and ra.bonus == rb.bonus
+
+
 @pytest.mark.parametrize("N,Hq,Hkv,D,P,norm", [(64, 32, 8, 128, 4096, True), (33, 4, 2, 64, 100, True),
                                                 (7, 40, 8, 128, 8192, False), (1, 2, 1, 64, 0, True),
                                                 (16, 8, 2, 128, 45000, True)])
