@@ -293,3 +293,21 @@ def test_decode_loop_threaded_hint():
     _check_margins(ref)
     _compare(recs, ref)
     print(f"  hint first seen at round {s}", flush=True)
+
+
+def test_decode_loop_stops_at_a_full_cache():
+    """With room for only a few rounds the loop stops before the prefix
+    plus a full trie would pass the cache, and a further round is refused
+    on the host; every committed row stays within the capacity."""
+    print("case decode loop full cache", flush=True)
+    case = _case(SEED, rounds_greedy=4)
+    cfg = dataclasses.replace(case.cfg, cap=case.cfg.prefix_len + case.cfg.max_nodes + 30)
+    case.cfg = cfg
+    case.kv = [mw.prefix_kv(cfg, SEED, l) for l in range(cfg.n_layers)]
+    loop, recs, _, _ = _gpu_loop(case, SidecarHint(_ChecksUntilReady(case.views, 0), cfg.vocab - 1), 100,
+                                 graphs=True)
+    assert recs and not loop.can_continue()
+    assert loop.P > cfg.cap - cfg.max_nodes and loop.P <= cfg.cap
+    assert recs[-1].prefix_len <= cfg.cap - cfg.max_nodes
+    with pytest.raises(RuntimeError):
+        loop.round()
