@@ -45,6 +45,8 @@ class SidecarHint:
     blocks: it returns None while the future is pending; the first poll that
     finds it done joins the views into one bank, each view followed by the
     EOS token, and every later poll returns that same array (encoded once).
+    A sidecar that failed (``result()`` raised, or views that are not token
+    sequences) is treated as never ready: the target does not depend on it.
     """
 
     def __init__(self, future, eos_token: int):
@@ -52,15 +54,22 @@ class SidecarHint:
         self.eos = int(eos_token)
         self.bank: Optional[np.ndarray] = None
         self.first_ready_round: Optional[int] = None
+        self.failed: Optional[BaseException] = None
 
     def poll(self, round_index: int) -> Optional[np.ndarray]:
-        if self.bank is None and self.future is not None and self.future.done():
-            views = self.future.result()
-            parts: List[int] = []
-            for v in views:
-                parts.extend(int(t) for t in v)
-                parts.append(self.eos)
-            self.bank = np.asarray(parts, dtype=np.int32)
+        if self.bank is None and self.failed is None and self.future is not None and self.future.done():
+            try:
+                parts: List[int] = []
+                for v in self.future.result():
+                    parts.extend(int(t) for t in v)
+                    parts.append(self.eos)
+                bank = np.asarray(parts, dtype=np.int32)
+                if (bank < 0).any():
+                    raise ValueError("negative token in the hint")
+            except Exception as e:  # a failed sidecar never delays or stops the target
+                self.failed = e
+                return None
+            self.bank = bank
             self.first_ready_round = round_index
         return self.bank
 

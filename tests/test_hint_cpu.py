@@ -144,3 +144,43 @@ def test_hint_bank_reproduces_the_candidate_lanes(name):
         assert r["suffix_len"] == 7 and r["n_hint"] >= 1
         assert _lanes(r)[0] == hint and lanes[0] == hint
         assert _lanes(r) == lanes
+
+
+# ----------------------------------------------------------------------------
+# the sidecar's future at the candidate boundary (Eq. 3): never blocks, bank
+# built once, a failed sidecar is never ready
+
+
+class _Fut:
+    def __init__(self, views=None, ready_after=0, exc=None):
+        self.views, self.ready_after, self.exc = views, ready_after, exc
+        self.done_calls = self.result_calls = 0
+
+    def done(self):
+        self.done_calls += 1
+        return self.done_calls > self.ready_after
+
+    def result(self):
+        self.result_calls += 1
+        if self.exc is not None:
+            raise self.exc
+        return self.views
+
+
+def test_sidecar_hint_pending_then_ready_once():
+    from paper_2608_00814_amd.decode import SidecarHint
+    f = _Fut(views=[[5, 6, 7], [], [8]], ready_after=2)
+    h = SidecarHint(f, eos_token=99)
+    assert h.poll(0) is None and h.poll(1) is None
+    b = h.poll(2)
+    assert b.tolist() == [5, 6, 7, 99, 99, 8, 99] and h.first_ready_round == 2
+    assert h.poll(3) is b and h.poll(4) is b and f.result_calls == 1
+
+
+def test_sidecar_hint_failure_is_never_ready():
+    from paper_2608_00814_amd.decode import SidecarHint
+    h = SidecarHint(_Fut(exc=RuntimeError("sidecar crashed")), eos_token=99)
+    assert all(h.poll(r) is None for r in range(4)) and isinstance(h.failed, RuntimeError)
+    h2 = SidecarHint(_Fut(views=[[1, -3]]), eos_token=99)
+    assert h2.poll(0) is None and h2.failed is not None and h2.poll(1) is None
+    assert SidecarHint(None, eos_token=99).poll(0) is None
