@@ -399,6 +399,7 @@ def bench_model(args):
 
 DECODE_METRIC = ("decode tokens/s (greedy, batch 1, asynchronous hint), Qwen3-8B decoder (36 layers, random "
                  "weights), 64-node tries, 4k prefix")
+HIDDEN_PUSH = 12.0  # planted LM-head rows: N(0,1) noise plus this times the unit W row of the greedy token
 DECODE_WORKLOADS = {"qwen3-8b-decode": "qwen3-8b-model", "small-decode": "small-model"}
 DECODE_TOKENS = 256       # tokens generated per request
 DECODE_HINT_DELAY_MS = 20  # the sidecar's hint arrives this long after the request starts
@@ -585,6 +586,138 @@ def bench_decode(args):
     print(json.dumps(out), flush=True)
 
 
+LOOP_METRIC = "decode verify steps/s over consecutive steps with compaction (wall clock, per-step host sync)"
+
+
+def bench_path_loop(args):
+    """Consecutive verify steps of the path with compaction, each step's root
+    the previous step's bonus token and the prefix growing by L + 1, timed by
+    the wall clock over all steps including the per-step synchronisation.
+    One captured graph per trie size, replayed with the prefix length read
+    from device memory.  Per step the host builds the step's candidates with
+    the workload generator (a stand-in for the schema chain, retrieved calls
+    and, from step 30 on, the hint), packs them and stages the planted
+    LM-head rows; the node queries and K/V rows are not restaged (their
+    values do not change the work)."""
+    import torch
+
+    from paper_2608_00814_amd import ooo
+    from paper_2608_00814_amd import workload as wl
+    from paper_2608_00814_amd.step import VerifyRunner
+
+    ooo.lib()
+    cfg = wl.CONFIGS[args.workload]
+    steps = args.steps if args.steps > 0 else cfg.steps
+    dev = torch.device("cuda:0")
+    seed = 0
+    t_setup = time.time()
+    bound = cfg.cap - cfg.max_nodes
+    runner = VerifyRunner(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.hidden, cfg.vocab,
+                          cfg.max_nodes, cfg.max_depth, torch.bfloat16, dev, max_prefix=bound)
+    w = wl.lm_head_weight(cfg, seed)
+    w_rows = torch.from_numpy(np.ascontiguousarray(w).view(np.int16)).view(torch.bfloat16).to(dev)
+    del w
+    runner.set_weight(w_rows.clone())
+    inv_norm = torch.rsqrt((w_rows.float() ** 2).sum(1))  # staging: X rows pushed along W[tau] / |W[tau]|
+    g = torch.Generator(device=dev).manual_seed(seed)
+    z = torch.randn(cfg.max_nodes, cfg.hidden, device=dev, generator=g)
+    x_buf = torch.empty(cfg.max_nodes, cfg.hidden, dtype=torch.bfloat16, device=dev)
+    shp = (cfg.n_layers, cfg.n_kv_heads, cfg.cap, cfg.head_dim)
+    k_cache = torch.randn(shp, device=dev, generator=g).to(torch.bfloat16)
+    v_cache = torch.randn(shp, device=dev, generator=g).to(torch.bfloat16)
+    q_layers = [torch.randn(cfg.max_nodes, cfg.n_q_heads, cfg.head_dim, device=dev, generator=g).to(torch.bfloat16)
+                for _ in range(cfg.n_layers)]
+    for n in range(1, cfg.max_nodes + 1):
+        runner.ensure_workspace(bound, n)
+    ws_ptr = runner.attn_ws.data_ptr()
+    torch.cuda.synchronize()
+    setup_s = time.time() - t_setup
+    stream = torch.cuda.Stream()
+    graphs = {}
+    done = torch.cuda.Event()
+
+    def run(n_steps):
+        root = wl.candidates_for(cfg, seed, 0).root_token
+        P = cfg.prefix_len
+        gen_s = dev_s = 0.0
+        Ls, mismatch, captures = [], 0, 0
+        for s_ in range(n_steps):
+            t0 = time.perf_counter()
+            cands = wl.candidates_for(cfg, seed, s_, root_token=root)
+            packed = runner.pack(root, *cands.csr())
+            tau, d = wl.designated_tokens(cfg, seed, s_, cands, packed["token"], packed["parent"])
+            t1 = time.perf_counter()
+            N = packed["n_nodes"]
+            with torch.cuda.stream(stream):
+                tdev = torch.from_numpy(tau.astype(np.int64)).to(dev, non_blocking=False)
+                x_buf[:N].copy_(z[:N] + HIDDEN_PUSH * w_rows[tdev].float() * inv_norm[tdev][:, None])
+                runner.set_prefix(P)
+                gr = graphs.get(N)
+                if gr is None:
+                    if runner.attn_ws.data_ptr() != ws_ptr:
+                        raise RuntimeError("attention workspace moved after a capture")
+                    gr = torch.cuda.CUDAGraph()
+                    with torch.cuda.graph(gr, stream=stream):
+                        runner.device_step(q_layers, k_cache, v_cache, x_buf, bound, prefix_dev=runner.prefix_dev)
+                    graphs[N] = gr
+                    captures += 1
+                gr.replay()
+                done.record(stream)
+            done.synchronize()
+            res = runner.result()
+            t2 = time.perf_counter()
+            gen_s += t1 - t0
+            dev_s += t2 - t1
+            mismatch += res.L != d
+            Ls.append(res.L)
+            root = res.bonus
+            P += res.L + 1
+            if P > bound:
+                break
+        return {"Ls": Ls, "gen_s": gen_s, "dev_s": dev_s, "mismatch": mismatch, "captures": captures, "P": P}
+
+    run(min(steps, max(args.warmup, 35)))  # captures the graphs of the trie sizes the steps produce
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    r = run(steps)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    n_done = len(r["Ls"])
+    committed = int(np.sum(np.array(r["Ls"]) + 1))
+    out = {
+        "metric": LOOP_METRIC,
+        "value": round(n_done / elapsed, 2),
+        "unit": "verify steps/s",
+        "n_gpus": 1,
+        "steps": n_done,
+        "warmup": max(args.warmup, 35),
+        "ms_per_step": round(1e3 * elapsed / n_done, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (generator candidates per step, planted acceptance)",
+        "config": {"workload": f"{cfg.name}: {cfg.description}", "n_layers": cfg.n_layers, "q_heads": cfg.n_q_heads,
+                   "kv_heads": cfg.n_kv_heads, "head_dim": cfg.head_dim, "prefix_len": cfg.prefix_len,
+                   "final_prefix_len": r["P"], "trie_nodes": cfg.max_nodes, "hidden": cfg.hidden,
+                   "vocab": cfg.vocab, "launch": "one hip-graph per trie size, prefix from device memory"},
+        "tokens_per_s": round(committed / elapsed, 1),
+        "mean_accepted_plus_bonus": round(committed / n_done, 3),
+        "generator_ms_per_step": round(1e3 * r["gen_s"] / n_done, 3),
+        "staging_and_device_ms_per_step": round(1e3 * r["dev_s"] / n_done, 3),
+        "steps_accepting_other_than_planted": r["mismatch"],
+        "graph_captures_in_timed_steps": r["captures"],
+        "roofline": None,
+        "setup_s": round(setup_s, 1),
+    }
+    if not args.no_cpu_baseline:
+        del k_cache, v_cache, q_layers, runner, graphs
+        torch.cuda.empty_cache()
+        cb = cpu_baseline(cfg, args.cpu_seconds)
+        out["cpu_baseline"] = cb
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -594,6 +727,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="launch every kernel eagerly")
+    ap.add_argument("--loop", action="store_true",
+                    help="consecutive verify steps with compaction from the workload's prefix (wall clock)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="one plain copy of this many MiB after setup (byte-counter calibration)")
     args = ap.parse_args()
@@ -608,6 +743,9 @@ def main():
         return
     if args.workload in DECODE_WORKLOADS:
         bench_decode(args)
+        return
+    if args.loop:
+        bench_path_loop(args)
         return
 
     import torch

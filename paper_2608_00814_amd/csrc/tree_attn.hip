@@ -10,9 +10,10 @@
 //    tiles).  Key tiles are 64 rows: the prefix tiles first, then the tree
 //    tiles [P, P+N) where the ancestor bitmask is tested in registers.
 //    A split is a fixed-length run of tiles, so the key ranges a row's
-//    partial sums cover (and its rounding) do not depend on how many rows
-//    share the launch: for a given key layout a node's output is bitwise
-//    the same in tries of any size.
+//    partial sums cover (and its rounding) do not depend on the row block:
+//    for a given key layout a node's output is bitwise the same in tries of
+//    any size that get the same split count (the count depends on the trie
+//    size only where the CUs limit it).
 //  * Scores are computed transposed, S^T = K Q^T, and the output as
 //    O^T = V^T P^T.  With the A-operand rows of K permuted (bits 2 and 3 of
 //    the row index swapped) every lane ends up holding one query row: its
@@ -192,12 +193,15 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
   const int P = a.P_dev ? __builtin_amdgcn_readfirstlane(min(max(*a.P_dev, 0), a.P)) : a.P;
   const int tiles_prefix = (P + kTile - 1) / kTile;
   const int tiles_total = tiles_prefix + (a.N + kTile - 1) / kTile;
-  // Fixed runs of tiles: a row's key ranges, and so its rounding, are the
-  // same whatever the trie size and the row block.  >= 1 tile when the
-  // plan's prefix is the actual one; a shorter device prefix can leave
-  // splits empty (handled below).
-  const int t_begin = s * a.tps;
-  const int t_end = min(t_begin + a.tps, tiles_total);
+  // Fixed-length runs of tiles, the length set by the actual prefix (with
+  // a device prefix the plan's split count is spread over the tiles the
+  // prefix has; with the launch value this is the plan's length), so a
+  // row's key ranges and its rounding do not depend on the row block.  The
+  // last splits can be empty when there are fewer tiles than splits
+  // (handled below).
+  const int tps = a.P_dev ? (tiles_total + a.splits - 1) / a.splits : a.tps;
+  const int t_begin = s * tps;
+  const int t_end = min(t_begin + tps, tiles_total);
   const int ntiles = t_end - t_begin;
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
