@@ -184,7 +184,7 @@ def _par(fn, items):
 
 def run_decode(name: str = "llama3.1-8b-decode", seed: int = 0, steps: Optional[int] = None,
                attn_steps: Sequence[int] = (0, 29, 30, 199), attn_layers: Sequence[int] = (0, 15, 31),
-               sample_rows: int = 6, verbose: bool = False) -> Dict:
+               sample_rows: int = 6, verbose: bool = False, graphs: bool = False) -> Dict:
     """Consecutive verification steps with compaction, each step's root the
     previous step's bonus token and the prefix growing by L+1.  Every step:
     the trie matches the reference packing, the greedy token of every node
@@ -229,6 +229,18 @@ def run_decode(name: str = "llama3.1-8b-decode", seed: int = 0, steps: Optional[
     total_tokens = 0
     worst_attn = worst_logit = 0.0
     rs = np.random.default_rng(seed + 2000)
+    if graphs:
+        # one captured step per trie size, replayed with the prefix length in
+        # device memory; the step's inputs go to fixed buffers first
+        bound = cfg.cap - cfg.max_nodes
+        for n in range(1, cfg.max_nodes + 1):
+            runner.ensure_workspace(bound, n)
+        q_fix = [torch.empty(cfg.max_nodes, cfg.n_q_heads, cfg.head_dim, dtype=tdt, device=dev)
+                 for _ in range(cfg.n_layers)]
+        x_fix = torch.empty(cfg.max_nodes, cfg.hidden, dtype=tdt, device=dev)
+        logits_fix = torch.empty(cfg.max_nodes, cfg.vocab, dtype=torch.float32, device=dev)
+        captured: Dict[int, torch.cuda.CUDAGraph] = {}
+        gstream = torch.cuda.Stream(device=dev)
     for step in range(steps):
         cands = wl.candidates_for(cfg, seed, step, root_token=root)
         tree = ov.pack_tree(cands.root_token, cands.seqs, cands.max_nodes, cands.max_depth)
@@ -249,8 +261,27 @@ def run_decode(name: str = "llama3.1-8b-decode", seed: int = 0, steps: Optional[
         q_dev = [to_dev(q, dt, dev) for q in qs]
         check_now = step in attn_steps
         logits_dev = torch.empty(N, cfg.vocab, dtype=torch.float32, device=dev) if check_now else None
-        runner.ensure_workspace(P)
-        runner.device_step(q_dev, k_dev, v_dev, to_dev(x, dt, dev), P, logits=logits_dev, compact=True)
+        if graphs:
+            for l in range(cfg.n_layers):
+                q_fix[l][:N].copy_(q_dev[l])
+            x_fix[:N].copy_(to_dev(x, dt, dev))
+            runner.set_prefix(P)
+            torch.cuda.synchronize()
+            with torch.cuda.stream(gstream):
+                gr = captured.get(N)
+                if gr is None:
+                    gr = torch.cuda.CUDAGraph()
+                    with torch.cuda.graph(gr, stream=gstream):
+                        runner.device_step(q_fix, k_dev, v_dev, x_fix, bound, logits=logits_fix[:N], compact=True,
+                                           prefix_dev=runner.prefix_dev)
+                    captured[N] = gr
+                gr.replay()
+            torch.cuda.synchronize()
+            if logits_dev is not None:
+                logits_dev.copy_(logits_fix[:N])
+        else:
+            runner.ensure_workspace(P)
+            runner.device_step(q_dev, k_dev, v_dev, to_dev(x, dt, dev), P, logits=logits_dev, compact=True)
         torch.cuda.synchronize()
         res = runner.result()
         ids = runner.ids[:N].cpu().numpy()

@@ -65,6 +65,15 @@ def test_decode_llama31_8b_200_steps():
     assert r["steps"] == 200 and r["final_prefix"] == 32768 + r["tokens"]
 
 
+def test_decode_llama31_8b_graph_replay_device_prefix():
+    """The same steps with one captured graph per trie size replayed with the
+    prefix length in device memory (what the decode loop and bench.py --loop
+    do): 40 steps, across the hint branch's start at step 30."""
+    print("case decode llama3.1-8b 40 steps, graphs + device prefix", flush=True)
+    r = gh.run_decode("llama3.1-8b-decode", seed=1, steps=40, attn_steps=(0, 29, 30, 39), verbose=True, graphs=True)
+    assert r["steps"] == 40 and r["final_prefix"] == 32768 + r["tokens"]
+
+
 def test_step_qwen25_32b_sampled():
     print("case qwen2.5-32b seed=0 (layers 0, 63 full; sampled rows elsewhere)", flush=True)
     gh.run_and_check("qwen2.5-32b", seed=0, layers=[0, 63], sample_rows=4, verbose=True)
