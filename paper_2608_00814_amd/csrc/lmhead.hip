@@ -145,7 +145,7 @@ __global__ __launch_bounds__(448) void lmhead_bf16_kernel(const uint16_t* __rest
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj)
               __builtin_amdgcn_global_load_lds(OOO_GLB(src + (sstep[s4] ? jj * 512 : 0)),
-                                               OOO_LDS(dst + (4 * s4 + jj) * 1024), 16, 0, 0);
+                                               OOO_LDS(dst + (4 * s4 + jj) * 1024), 16, 0, kStreamOnce);
           } else {
             const int gi = group_of(t, s4);
 #pragma unroll
@@ -154,7 +154,7 @@ __global__ __launch_bounds__(448) void lmhead_bf16_kernel(const uint16_t* __rest
               const int pc = (lane % 8) ^ (r % 8);
               const int row = min(32 * gi + r, V - 1);
               __builtin_amdgcn_global_load_lds(OOO_GLB(Wt + (size_t)row * H + kc * 64 + pc * 8),
-                                               OOO_LDS(dst + (4 * s4 + jj) * 1024), 16, 0, 0);
+                                               OOO_LDS(dst + (4 * s4 + jj) * 1024), 16, 0, kStreamOnce);
             }
           }
         }

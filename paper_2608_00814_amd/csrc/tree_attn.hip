@@ -93,6 +93,15 @@ __device__ __forceinline__ void dma16(const void* base, uint32_t voff, uint32_t 
                : "memory", "m0");
 }
 
+// Same with the non-temporal (streaming) cache policy, for the K/V tiles:
+// each head's K/V stream is read once per row block, and keeping it from
+// displacing the rest of the L2 (the queries every split re-reads, the
+// partials) measured 16.6 -> 15.5 us per call at the Qwen3-8B shape.
+__device__ __forceinline__ void dma16_nt(const void* base, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2 nt" ::"s"(lds), "v"(voff), "s"(base)
+               : "memory", "m0");
+}
+
 // Same for 4 bytes per lane (lane l's dword lands at lds + 4*l).
 __device__ __forceinline__ void dma4(const void* base, uint32_t voff, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, %2" ::"s"(lds), "v"(voff), "s"(base)
@@ -270,17 +279,17 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
     const uint32_t kl = lds_addr(kst[ST]) + wave_u * 1024, vl = lds_addr(vst[ST]) + wave_u * 1024;
     if (row0 + kTile <= limit) {
 #pragma unroll
-      for (int i = 0; i < PM; ++i) dma16(kb, dvoff[i], kl + i * NW * 1024);
+      for (int i = 0; i < PM; ++i) dma16_nt(kb, dvoff[i], kl + i * NW * 1024);
 #pragma unroll
-      for (int i = 0; i < PM; ++i) dma16(vb, dvoff[i], vl + i * NW * 1024);
+      for (int i = 0; i < PM; ++i) dma16_nt(vb, dvoff[i], vl + i * NW * 1024);
     } else {
 #pragma unroll
       for (int i = 0; i < PM; ++i) {
         const int r = (i * NW + wave) * R::RPI + lane / R::CH;
         const int rc = min(r, limit - 1 - row0);
         const uint32_t vo = rc * R::ROWB + R::swz(r, lane % R::CH) * 16;
-        dma16(kb, vo, kl + i * NW * 1024);
-        dma16(vb, vo, vl + i * NW * 1024);
+        dma16_nt(kb, vo, kl + i * NW * 1024);
+        dma16_nt(vb, vo, vl + i * NW * 1024);
       }
     }
   };
