@@ -18,9 +18,10 @@ constexpr int kWave = 64;
 // Cache-policy operand of a global load whose data is read exactly once:
 // the non-temporal (streaming) bit, so the stream does not displace data
 // that is reused, such as the activation chunks every block re-reads, from
-// the L2.  Used for the LM-head weight (1.25 GB per step: 209 -> 188 us);
-// measured slightly slower for the smaller projection weights, which keep
-// the default policy.
+// the L2.  LM-head weight: 209 -> 188 us per call; projection weights:
+// 182.8 -> 183.9 full-model steps/s (a microbenchmark cycling through a few
+// weights that fit the last-level cache showed the opposite, which a model
+// streaming 13.9 GB per step does not see).
 constexpr int kStreamOnce = 2;
 
 __device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) {

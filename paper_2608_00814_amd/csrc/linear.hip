@@ -106,7 +106,8 @@ __global__ __launch_bounds__(448) void linear_bf16_kernel(const uint16_t* __rest
           const uint16_t* src = Wt + ((size_t)t * KC + kc) * (kRows * 64) + half * (kRows * 32) + lane * 8;
 #pragma unroll
           for (int j = 0; j < R::WDMA; ++j)
-            __builtin_amdgcn_global_load_lds(OOO_GLB(src + j * 512), OOO_LDS(dst + j * 1024), 16, 0, 0);
+            __builtin_amdgcn_global_load_lds(OOO_GLB(src + j * 512), OOO_LDS(dst + j * 1024), 16, 0,
+                                             kStreamOnce);
         } else {
 #pragma unroll
           for (int j = 0; j < R::WDMA; ++j) {
@@ -114,7 +115,7 @@ __global__ __launch_bounds__(448) void linear_bf16_kernel(const uint16_t* __rest
             const int pc = (lane % 8) ^ (r % 8);
             const int row = min(t * kRows + r, O - 1);
             __builtin_amdgcn_global_load_lds(OOO_GLB(Wt + (size_t)row * K + kc * 64 + pc * 8),
-                                             OOO_LDS(dst + j * 1024), 16, 0, 0);
+                                             OOO_LDS(dst + j * 1024), 16, 0, kStreamOnce);
           }
         }
       } else {
