@@ -740,8 +740,13 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
 // owns row c and the 8 columns 32(k/2) + 16(k%2) + 4u + {0..3, 8..11}.
 // Every load is issued before any arithmetic (one round trip to memory):
 // splits past the count re-read the last split and get weight zero.
+// Waves per combine workgroup.  Two rather than four spreads the partial
+// reads over twice as many CUs: 15.95 -> 15.75 us per call (main kernel plus
+// combine) at the Qwen3-8B shape (64 nodes, 4k prefix, 13 splits).
+constexpr int kCombineWaves = 2;
+
 template <int D, int SMAX>
-__global__ __launch_bounds__(256) void tree_attn_combine_kernel(AttnArgs a) {
+__global__ __launch_bounds__(64 * kCombineWaves) void tree_attn_combine_kernel(AttnArgs a) {
   constexpr int NP = D / 16;  // group pairs per lane
   const int lane = threadIdx.x & 63;
   // Same XCD-aware order as the main kernel: the blocks that share
@@ -749,7 +754,7 @@ __global__ __launch_bounds__(256) void tree_attn_combine_kernel(AttnArgs a) {
   // range whose partials that XCD wrote, so the loads hit its L2.
   int b = blockIdx.x;
   if (gridDim.x % 8 == 0) b = (b % 8) * (gridDim.x / 8) + b / 8;
-  const int wv = b * 4 + (threadIdx.x >> 6);
+  const int wv = b * kCombineWaves + (threadIdx.x >> 6);
   const int nblk = a.Mpad / 32;
   if (wv >= a.Hkv * nblk * NP) return;
   const int k = wv % NP, blk = (wv / NP) % nblk, g = wv / (NP * nblk);
@@ -1010,15 +1015,15 @@ extern "C" int ooo_tree_attn(const void* q, const void* k_cache, const void* v_c
     }
     if (p.splits > 1) {
       const int waves = n_kv_heads * (p.Mpad / 32) * (head_dim / 16);
-      const dim3 cgrid((waves + 3) / 4);
+      const dim3 cgrid((waves + kCombineWaves - 1) / kCombineWaves);
       if (head_dim == 128) {
-        if (p.splits <= 8) tree_attn_combine_kernel<128, 8><<<cgrid, 256, 0, st>>>(a);
-        else if (p.splits <= 16) tree_attn_combine_kernel<128, 16><<<cgrid, 256, 0, st>>>(a);
-        else tree_attn_combine_kernel<128, 32><<<cgrid, 256, 0, st>>>(a);
+        if (p.splits <= 8) tree_attn_combine_kernel<128, 8><<<cgrid, 64 * kCombineWaves, 0, st>>>(a);
+        else if (p.splits <= 16) tree_attn_combine_kernel<128, 16><<<cgrid, 64 * kCombineWaves, 0, st>>>(a);
+        else tree_attn_combine_kernel<128, 32><<<cgrid, 64 * kCombineWaves, 0, st>>>(a);
       } else {
-        if (p.splits <= 8) tree_attn_combine_kernel<64, 8><<<cgrid, 256, 0, st>>>(a);
-        else if (p.splits <= 16) tree_attn_combine_kernel<64, 16><<<cgrid, 256, 0, st>>>(a);
-        else tree_attn_combine_kernel<64, 32><<<cgrid, 256, 0, st>>>(a);
+        if (p.splits <= 8) tree_attn_combine_kernel<64, 8><<<cgrid, 64 * kCombineWaves, 0, st>>>(a);
+        else if (p.splits <= 16) tree_attn_combine_kernel<64, 16><<<cgrid, 64 * kCombineWaves, 0, st>>>(a);
+        else tree_attn_combine_kernel<64, 32><<<cgrid, 64 * kCombineWaves, 0, st>>>(a);
       }
     }
   }
