@@ -169,8 +169,12 @@ int ooo_hint_merge(const int32_t* bank, int64_t bank_len, int32_t eos_token, con
  * Query head h reads KV head h / (n_q_heads / n_kv_heads).  For node i the
  * keys are prefix rows 0..P-1 and rows P + j for every j set in anc_mask[i];
  * softmax in float32.
- * Supported: head_dim 64 or 128; n_q_heads / n_kv_heads <= 8 for OOO_BF16;
+ * Supported: head_dim 64 or 128; any n_q_heads / n_kv_heads;
  * n_nodes <= 64 * mask_words <= 1024.
+ * Two environment variables, read at each call, exist for tests and tuning:
+ * OOO_ATTN_SPLITS forces the bf16 split count (clamped to 1..32 and to the
+ * key tiles), OOO_ATTN_SPLITK=0 selects the one-wave-per-row-group bf16
+ * kernel at head_dim 128; results stay within the same tolerance.
  * Errors: OOO_ERR_INVALID (null pointers, n_nodes < 1, prefix_len < 0,
  * P + n_nodes > cap, n_q_heads % n_kv_heads != 0, 64 * mask_words < n_nodes),
  * OOO_ERR_UNSUPPORTED, OOO_ERR_CAPACITY (ws_bytes below the query),

@@ -113,7 +113,7 @@ class VerifyRunner:
         n = self.n_nodes if n_nodes is None else n_nodes
         need = ooo.tree_attn_workspace(max(n, 1), self.Hq, self.Hkv, self.D, prefix_len, self.code)
         if need > self.attn_ws.numel() * 4:
-            self.attn_ws = torch.zeros(need // 4 + 1, dtype=torch.float32, device=self.device)  # counters start at 0
+            self.attn_ws = torch.zeros(need // 4 + 1, dtype=torch.float32, device=self.device)
 
     # -- device -------------------------------------------------------------
     def upload_tree(self, stream=None) -> None:

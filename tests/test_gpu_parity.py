@@ -114,6 +114,8 @@ ATTN_CASES = [
     (200, 200, 3, 3, 128, "random", "bf16"),
     (4096, 64, 4, 8, 128, "random", "bf16"),
     (77, 300, 2, 1, 64, "random", "bf16"),
+    (500, 40, 16, 1, 128, "random", "bf16"),
+    (100, 9, 12, 2, 64, "deep", "bf16"),
     (128, 25, 4, 1, 64, "random", "f32"),
     (1, 40, 2, 2, 128, "deep", "f32"),
     (0, 3, 1, 1, 64, "star", "f32"),
@@ -139,7 +141,7 @@ def _run_attn(q, k, v, P, N, mask, Hq, Hkv, D, dt):
     md = torch.from_numpy(mask.view(np.int64)).to(DEV)
     out = torch.full((N, Hq, D), float("nan"), dtype=tdt, device=DEV)
     ws_n = ooo.tree_attn_workspace(N, Hq, Hkv, D, P, code)
-    ws = torch.zeros(max(ws_n, 4) // 4 + 1, dtype=torch.float32, device=DEV)  # split counters start at 0
+    ws = torch.zeros(max(ws_n, 4) // 4 + 1, dtype=torch.float32, device=DEV)
     ooo.tree_attn(qd, kd, vd, P, N, md, Hq, Hkv, 1.0 / math.sqrt(D), out, ws)
     torch.cuda.synchronize()
     return gh.wl.to_f64(gh.to_host(out, dt), dt)
