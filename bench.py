@@ -385,7 +385,8 @@ def bench_model(args):
         "roofline": {"bound": "hbm", "kernel": ("projections over all layers (qkv with norms/rotation, o_proj and down with residual add + "
                                 "RMSNorm, gate+up with SwiGLU; streaming + epilogue kernels)"),
                      "achieved": round(proj_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(proj_gbs / HBM_PEAK_GBS, 4), "traffic": None, "bytes_per_launch": w_bytes,
+                     "frac": round(proj_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": recorded_traffic(mcfg.name, "projections"), "bytes_per_launch": w_bytes,
                      "us_per_launch": phase["projections_us"]},
         "step_weight_gbs": round(w_bytes / step_s / 1e9, 1),
         "setup_s": round(setup_s, 1),
