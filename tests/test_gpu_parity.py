@@ -116,11 +116,15 @@ ATTN_CASES = [
     (77, 300, 2, 1, 64, "random", "bf16"),
     (500, 40, 16, 1, 128, "random", "bf16"),
     (100, 9, 12, 2, 64, "deep", "bf16"),
+    # the largest tries the boundary takes (16 ancestor-mask words)
+    (100, 1024, 1, 1, 64, "random", "bf16"),
+    (37, 700, 2, 1, 128, "deep", "bf16"),
     (128, 25, 4, 1, 64, "random", "f32"),
     (1, 40, 2, 2, 128, "deep", "f32"),
     (0, 3, 1, 1, 64, "star", "f32"),
     (3000, 70, 4, 2, 128, "random", "f32"),
     (255, 2, 2, 1, 64, "chain", "f32"),
+    (10, 1000, 1, 1, 64, "random", "f32"),
 ]
 
 
