@@ -56,7 +56,8 @@ def test_rmsnorm(N, H):
 
 
 @pytest.mark.parametrize("N,K,O", [(64, 4096, 6144), (64, 4096, 4096), (37, 4096, 24576), (64, 12288, 4096),
-                                   (1, 256, 1152), (5, 512, 256), (200, 1024, 3000), (33, 64, 130)])
+                                   (1, 256, 1152), (5, 512, 256), (200, 1024, 3000), (33, 64, 130),
+                                   (256, 512, 768), (129, 320, 512)])
 @pytest.mark.parametrize("packed", [True, False], ids=["packed", "rows"])
 def test_linear(N, K, O, packed):
     """Every epilogue of the streaming projection, both weight layouts, and
