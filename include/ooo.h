@@ -171,14 +171,19 @@ int ooo_hint_merge(const int32_t* bank, int64_t bank_len, int32_t eos_token, con
  * softmax in float32.
  * Supported: head_dim 64 or 128; any n_q_heads / n_kv_heads;
  * n_nodes <= 64 * mask_words <= 1024.
- * Two environment variables, read at each call, exist for tests and tuning:
- * OOO_ATTN_SPLITS forces the bf16 split count (clamped to 1..32 and to the
- * key tiles), OOO_ATTN_SPLITK=0 selects the one-wave-per-row-group bf16
- * kernel at head_dim 128; results stay within the same tolerance.
+ * workspace, ws_bytes  device scratch of ooo_tree_attn_workspace() bytes (0
+ *            when the plan needs none; then workspace may be NULL): the bf16
+ *            path splits the keys over workgroups, and a second kernel on the
+ *            same stream merges the splits' partial results from it.
  * Errors: OOO_ERR_INVALID (null pointers, n_nodes < 1, prefix_len < 0,
  * P + n_nodes > cap, n_q_heads % n_kv_heads != 0, 64 * mask_words < n_nodes),
  * OOO_ERR_UNSUPPORTED, OOO_ERR_CAPACITY (ws_bytes below the query),
  * OOO_ERR_HIP.
+ *
+ * Relative to the plain signature of this step (Q, the layer's K/V cache, P,
+ * N, the ancestor masks, head counts, scale, dtype, out, workspace, stream),
+ * two arguments are additions: prefix_len_dev (one captured step replayed as
+ * P grows) and the explicit head_dim.
  */
 size_t ooo_tree_attn_workspace(int32_t n_nodes, int32_t n_q_heads, int32_t n_kv_heads,
                                int32_t head_dim, int32_t prefix_len, ooo_dtype dt);
@@ -188,6 +193,24 @@ int ooo_tree_attn(const void* q, const void* k_cache, const void* v_cache, int64
                   int32_t mask_words, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
                   float scale, ooo_dtype dt, void* out, void* workspace, size_t ws_bytes,
                   void* stream);
+
+/*
+ * ooo_tree_attn_ex, ooo_tree_attn_workspace_ex - ooo_tree_attn with the
+ * planner's choices overridden, for tests and tuning.
+ *   force_splits  0: the planner's split count; > 0: that many key splits
+ *                 (clamped to 1..32 and to the key tiles)
+ *   variant       0: the default kernel; 1: one wave per 32-row group at
+ *                 head_dim 128 (the head_dim 64 kernel's scheme)
+ * Results stay within the same tolerance; each setting is deterministic.
+ * The workspace query must be made with the same force_splits.
+ */
+size_t ooo_tree_attn_workspace_ex(int32_t n_nodes, int32_t n_q_heads, int32_t n_kv_heads,
+                                  int32_t head_dim, int32_t prefix_len, ooo_dtype dt, int32_t force_splits);
+int ooo_tree_attn_ex(const void* q, const void* k_cache, const void* v_cache, int64_t cap,
+                     int32_t prefix_len, const int32_t* prefix_len_dev, int32_t n_nodes,
+                     const uint64_t* anc_mask, int32_t mask_words, int32_t n_q_heads, int32_t n_kv_heads,
+                     int32_t head_dim, float scale, ooo_dtype dt, void* out, void* workspace,
+                     size_t ws_bytes, void* stream, int32_t force_splits, int32_t variant);
 
 /*
  * ooo_lmhead_pack - one-time re-layout of the LM-head weight for streaming.

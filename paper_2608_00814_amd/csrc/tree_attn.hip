@@ -473,11 +473,14 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
     using I1 = std::integral_constant<int, 1>;
     using I2 = std::integral_constant<int, 2>;
     using I3 = std::integral_constant<int, 3>;
-    if (ntiles > 1) issue(t_begin + 1, I1{});
     // Tile 0 landed (the compiler does not track the DMA, so the barrier
-    // alone would not wait for it); the mask words in LDS are visible.
-    wait_tiles<PER, 1>(min(1, ntiles - 1));
+    // alone would not wait for it); the mask words in LDS are visible.  Tile
+    // 1 is requested only now: with every block asking for tiles 0 and 1 at
+    // once, each block's tile 0 lands later (15.57 -> 15.41 us per call at
+    // the Qwen3-8B shape, graphs of 36 calls).
+    wait_vmcnt<0>();
     __syncthreads();
+    if (ntiles > 1) issue(t_begin + 1, I1{});
     {
       const int rq = rg * 32 + c;
       const uint8_t* qs = (rg < 2 ? k3 : v3) + (rq % 64) * R::ROWB;
@@ -889,7 +892,8 @@ struct Plan {
   size_t ws_bytes;
 };
 
-Plan make_plan(int N, int Hq, int Hkv, int D, int P, ooo_dtype dt) {
+// force_splits > 0 replaces the planner's split count (tests and tuning).
+Plan make_plan(int N, int Hq, int Hkv, int D, int P, ooo_dtype dt, int force_splits) {
   Plan p{};
   if (dt != OOO_BF16) return p;
   const int G = Hq / Hkv;
@@ -910,7 +914,7 @@ Plan make_plan(int N, int Hq, int Hkv, int D, int P, ooo_dtype dt) {
     const int cost = 13 * ((p.tiles_total + sc - 1) / sc) + 5 * sc;
     if (cost < best) best = cost, splits = sc;
   }
-  if (const char* env = getenv("OOO_ATTN_SPLITS")) splits = atoi(env);
+  if (force_splits > 0) splits = force_splits;
   if (splits > 32) splits = 32;
   if (splits > p.tiles_total) splits = p.tiles_total;
   if (splits < 1) splits = 1;
@@ -927,18 +931,24 @@ Plan make_plan(int N, int Hq, int Hkv, int D, int P, ooo_dtype dt) {
 
 using namespace ooo;
 
-extern "C" size_t ooo_tree_attn_workspace(int32_t n_nodes, int32_t n_q_heads, int32_t n_kv_heads,
-                                          int32_t head_dim, int32_t prefix_len, ooo_dtype dt) {
+extern "C" size_t ooo_tree_attn_workspace_ex(int32_t n_nodes, int32_t n_q_heads, int32_t n_kv_heads,
+                                             int32_t head_dim, int32_t prefix_len, ooo_dtype dt,
+                                             int32_t force_splits) {
   if (n_nodes < 1 || n_kv_heads < 1 || n_q_heads < 1 || n_q_heads % n_kv_heads || prefix_len < 0) return 0;
-  return make_plan(n_nodes, n_q_heads, n_kv_heads, head_dim, prefix_len, dt).ws_bytes;
+  return make_plan(n_nodes, n_q_heads, n_kv_heads, head_dim, prefix_len, dt, force_splits).ws_bytes;
 }
 
-extern "C" int ooo_tree_attn(const void* q, const void* k_cache, const void* v_cache, int64_t cap,
-                             int32_t prefix_len, const int32_t* prefix_len_dev, int32_t n_nodes,
-                             const uint64_t* anc_mask,
-                             int32_t mask_words, int32_t n_q_heads, int32_t n_kv_heads,
-                             int32_t head_dim, float scale, ooo_dtype dt, void* out, void* workspace,
-                             size_t ws_bytes, void* stream) {
+extern "C" size_t ooo_tree_attn_workspace(int32_t n_nodes, int32_t n_q_heads, int32_t n_kv_heads,
+                                          int32_t head_dim, int32_t prefix_len, ooo_dtype dt) {
+  return ooo_tree_attn_workspace_ex(n_nodes, n_q_heads, n_kv_heads, head_dim, prefix_len, dt, 0);
+}
+
+extern "C" int ooo_tree_attn_ex(const void* q, const void* k_cache, const void* v_cache, int64_t cap,
+                                int32_t prefix_len, const int32_t* prefix_len_dev, int32_t n_nodes,
+                                const uint64_t* anc_mask, int32_t mask_words, int32_t n_q_heads,
+                                int32_t n_kv_heads, int32_t head_dim, float scale, ooo_dtype dt, void* out,
+                                void* workspace, size_t ws_bytes, void* stream, int32_t force_splits,
+                                int32_t variant) {
   OOO_REQUIRE(q && k_cache && v_cache && anc_mask && out, OOO_ERR_INVALID, "ooo_tree_attn: null pointer");
   OOO_REQUIRE(n_nodes >= 1, OOO_ERR_INVALID, "ooo_tree_attn: n_nodes must be >= 1");
   OOO_REQUIRE(prefix_len >= 0, OOO_ERR_INVALID, "ooo_tree_attn: prefix_len must be >= 0");
@@ -951,6 +961,8 @@ extern "C" int ooo_tree_attn(const void* q, const void* k_cache, const void* v_c
   OOO_REQUIRE(mask_words >= 1 && (int64_t)mask_words * 64 >= n_nodes && mask_words <= 16, OOO_ERR_INVALID,
               "ooo_tree_attn: mask_words=%d cannot describe %d nodes (max 16 words)", mask_words, n_nodes);
   OOO_REQUIRE(dt == OOO_F32 || dt == OOO_BF16, OOO_ERR_INVALID, "ooo_tree_attn: unknown dtype %d", (int)dt);
+  OOO_REQUIRE(force_splits >= 0 && (variant == 0 || variant == 1), OOO_ERR_INVALID,
+              "ooo_tree_attn: force_splits (%d) must be >= 0 and variant (%d) 0 or 1", force_splits, variant);
   OOO_REQUIRE(head_dim == 64 || head_dim == 128, OOO_ERR_UNSUPPORTED,
               "ooo_tree_attn: head_dim %d not supported (64 or 128)", head_dim);
   OOO_REQUIRE((int64_t)n_nodes * n_q_heads * head_dim * 2 < (1LL << 32), OOO_ERR_UNSUPPORTED,
@@ -969,7 +981,7 @@ extern "C" int ooo_tree_attn(const void* q, const void* k_cache, const void* v_c
                                                      cap, prefix_len, prefix_len_dev, n_nodes, anc_mask,
                                                      mask_words, n_q_heads, n_kv_heads, scale, (float*)out);
   } else {
-    const Plan p = make_plan(n_nodes, n_q_heads, n_kv_heads, head_dim, prefix_len, dt);
+    const Plan p = make_plan(n_nodes, n_q_heads, n_kv_heads, head_dim, prefix_len, dt, force_splits);
     OOO_REQUIRE(ws_bytes >= p.ws_bytes && (p.ws_bytes == 0 || workspace), OOO_ERR_CAPACITY,
                 "ooo_tree_attn: workspace of %zu bytes needed (got %zu)", p.ws_bytes, ws_bytes);
     AttnArgs a{};
@@ -1000,10 +1012,8 @@ extern "C" int ooo_tree_attn(const void* q, const void* k_cache, const void* v_c
     }
     const dim3 grid(n_kv_heads * p.row_blocks * p.splits);
     // head_dim 128 runs the key-split kernel (two waves per row group);
-    // OOO_ATTN_SPLITK=0 selects the one-wave pipelined kernel instead.
-    const char* sk_env = getenv("OOO_ATTN_SPLITK");
-    const bool splitk = !sk_env || atoi(sk_env) != 0;
-    if (head_dim == 128 && splitk) {
+    // variant 1 selects the one-wave pipelined kernel instead.
+    if (head_dim == 128 && variant == 0) {
       if (p.waves == 2) tree_attn_bf16_kernel<128, 2, true><<<grid, 256, 0, st>>>(a);
       else tree_attn_bf16_kernel<128, 4, true><<<grid, 512, 0, st>>>(a);
     } else if (head_dim == 128) {
@@ -1030,4 +1040,13 @@ extern "C" int ooo_tree_attn(const void* q, const void* k_cache, const void* v_c
   const hipError_t e = hipGetLastError();
   OOO_REQUIRE(e == hipSuccess, OOO_ERR_HIP, "ooo_tree_attn: launch failed: %s", hipGetErrorString(e));
   return ooo::ok();
+}
+
+extern "C" int ooo_tree_attn(const void* q, const void* k_cache, const void* v_cache, int64_t cap,
+                             int32_t prefix_len, const int32_t* prefix_len_dev, int32_t n_nodes,
+                             const uint64_t* anc_mask, int32_t mask_words, int32_t n_q_heads, int32_t n_kv_heads,
+                             int32_t head_dim, float scale, ooo_dtype dt, void* out, void* workspace,
+                             size_t ws_bytes, void* stream) {
+  return ooo_tree_attn_ex(q, k_cache, v_cache, cap, prefix_len, prefix_len_dev, n_nodes, anc_mask, mask_words,
+                          n_q_heads, n_kv_heads, head_dim, scale, dt, out, workspace, ws_bytes, stream, 0, 0);
 }

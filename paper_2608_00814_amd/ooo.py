@@ -40,6 +40,9 @@ SIGNATURES = {
     "ooo_tree_attn_workspace": (_sz, [_i32, _i32, _i32, _i32, _i32, ctypes.c_int]),
     "ooo_tree_attn": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _vp, _i32, _vp, _i32, _i32, _i32, _i32,
                                      ctypes.c_float, ctypes.c_int, _vp, _vp, _sz, _vp]),
+    "ooo_tree_attn_workspace_ex": (_sz, [_i32, _i32, _i32, _i32, _i32, ctypes.c_int, _i32]),
+    "ooo_tree_attn_ex": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _vp, _i32, _vp, _i32, _i32, _i32, _i32,
+                                        ctypes.c_float, ctypes.c_int, _vp, _vp, _sz, _vp, _i32, _i32]),
     "ooo_lmhead_workspace": (_sz, [_i32, _i32, _i32, ctypes.c_int]),
     "ooo_lmhead_packed_bytes": (_sz, [_i32, _i32, ctypes.c_int]),
     "ooo_lmhead_pack": (ctypes.c_int, [_vp, _i32, _i32, ctypes.c_int, _vp, _sz, _vp]),
@@ -256,25 +259,31 @@ def hint_merge(bank: np.ndarray, eos_token: int, committed: np.ndarray, native_t
 
 
 def tree_attn_workspace(n_nodes: int, n_q_heads: int, n_kv_heads: int, head_dim: int, prefix_len: int,
-                        dtype: int) -> int:
-    return int(lib().ooo_tree_attn_workspace(n_nodes, n_q_heads, n_kv_heads, head_dim, prefix_len, dtype))
+                        dtype: int, force_splits: int = 0) -> int:
+    """Bytes of attention workspace (``force_splits`` as for ``tree_attn``)."""
+    return int(lib().ooo_tree_attn_workspace_ex(n_nodes, n_q_heads, n_kv_heads, head_dim, prefix_len, dtype,
+                                                force_splits))
 
 
 def tree_attn(q, k_cache, v_cache, prefix_len: int, n_nodes: int, anc_mask, n_q_heads: int, n_kv_heads: int,
-              scale: float, out, workspace=None, stream=None, prefix_dev=None) -> None:
+              scale: float, out, workspace=None, stream=None, prefix_dev=None, force_splits: int = 0,
+              variant: int = 0) -> None:
     """q [N][Hq][D]; k_cache/v_cache one layer [Hkv][cap][D]; anc_mask
     [N][W] int64/uint64 device tensor; out [N][Hq][D].  ``prefix_dev``: an
     int32 device tensor whose first element is the prefix length used at run
-    time (``prefix_len`` bounds it), or None."""
+    time (``prefix_len`` bounds it), or None.  ``force_splits`` (> 0) and
+    ``variant`` (1: one wave per row group at head_dim 128) override the
+    planner, for tests and tuning."""
     for t, nm in ((q, "q"), (k_cache, "k_cache"), (v_cache, "v_cache"), (anc_mask, "anc_mask"), (out, "out")):
         _dev(t, nm)
     Hkv, cap, D = k_cache.shape
     W = anc_mask.shape[-1]
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    _check(lib().ooo_tree_attn(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), cap, prefix_len,
-                               _prefix_ptr(prefix_dev), n_nodes,
-                               anc_mask.data_ptr(), W, n_q_heads, n_kv_heads, D, float(scale), dtype_code(q),
-                               out.data_ptr(), _ptr(workspace), ws_bytes, _stream(stream)))
+    _check(lib().ooo_tree_attn_ex(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), cap, prefix_len,
+                                  _prefix_ptr(prefix_dev), n_nodes,
+                                  anc_mask.data_ptr(), W, n_q_heads, n_kv_heads, D, float(scale), dtype_code(q),
+                                  out.data_ptr(), _ptr(workspace), ws_bytes, _stream(stream), force_splits,
+                                  variant))
 
 
 def lmhead_workspace(n_nodes: int, hidden_dim: int, vocab: int, dtype: int) -> int:

@@ -2,6 +2,7 @@
 algorithmic byte counts the roofline divides by, and the lookup of the
 committed HBM-counter profiles."""
 
+import json
 import os
 import subprocess
 import sys
@@ -32,14 +33,22 @@ def test_algorithmic_bytes_at_the_qwen3_8b_shape():
     assert bench.lmhead_bytes(cfg, N) == 151936 * 4096 * 2 + 64 * 4096 * 2 + 64 * 8 == 1245184512
 
 
-def test_recorded_traffic_follows_the_sources(monkeypatch):
-    got = bench.recorded_traffic("qwen3-8b", "ooo_tree_attn")
-    assert got is not None and got >= bench.attention_bytes(wl.CONFIGS["qwen3-8b"], 64)
+def test_recorded_traffic_follows_the_sources(tmp_path, monkeypatch):
+    """A counter profile counts only while the kernel sources it names are
+    unchanged (comments aside)."""
+    src = "paper_2608_00814_amd/csrc/tree_attn.hip"
+    os.makedirs(tmp_path / "profiles")
+    os.makedirs(tmp_path / os.path.dirname(src))
+    (tmp_path / src).write_text(open(os.path.join(ROOT, src)).read())
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    rec = {"workload": "w", "ooo_tree_attn": {"bytes_per_launch": 123456, "sources": {src: bench._source_digest(src)}}}
+    (tmp_path / "profiles" / "hbm_traffic_w.json").write_text(json.dumps(rec))
+    assert bench.recorded_traffic("w", "ooo_tree_attn") == 123456
     assert bench.recorded_traffic("no-such-workload", "ooo_tree_attn") is None
-    assert bench.recorded_traffic("qwen3-8b", "no-such-entry") is None
+    assert bench.recorded_traffic("w", "no-such-entry") is None
     # a kernel source that changed since the counters were taken voids them
-    monkeypatch.setattr(bench, "_source_digest", lambda path: "0" * 16)
-    assert bench.recorded_traffic("qwen3-8b", "ooo_tree_attn") is None
+    (tmp_path / src).write_text(open(os.path.join(ROOT, src)).read() + "\nint x;\n")
+    assert bench.recorded_traffic("w", "ooo_tree_attn") is None
 
 
 @pytest.mark.parametrize("path", ["paper_2608_00814_amd/csrc/tree_attn.hip"])

@@ -138,15 +138,16 @@ def _attn_inputs(P, N, G, Hkv, D, dt, seed, pad=3):
     return rs, q, k, v, cap
 
 
-def _run_attn(q, k, v, P, N, mask, Hq, Hkv, D, dt):
+def _run_attn(q, k, v, P, N, mask, Hq, Hkv, D, dt, force_splits=0, variant=0):
     tdt = gh.torch_dtype(dt)
     code = ooo.BF16 if dt == "bf16" else ooo.F32
     qd, kd, vd = gh.to_dev(q, dt, DEV), gh.to_dev(k, dt, DEV), gh.to_dev(v, dt, DEV)
     md = torch.from_numpy(mask.view(np.int64)).to(DEV)
     out = torch.full((N, Hq, D), float("nan"), dtype=tdt, device=DEV)
-    ws_n = ooo.tree_attn_workspace(N, Hq, Hkv, D, P, code)
+    ws_n = ooo.tree_attn_workspace(N, Hq, Hkv, D, P, code, force_splits)
     ws = torch.zeros(max(ws_n, 4) // 4 + 1, dtype=torch.float32, device=DEV)
-    ooo.tree_attn(qd, kd, vd, P, N, md, Hq, Hkv, 1.0 / math.sqrt(D), out, ws)
+    ooo.tree_attn(qd, kd, vd, P, N, md, Hq, Hkv, 1.0 / math.sqrt(D), out, ws, force_splits=force_splits,
+                  variant=variant)
     torch.cuda.synchronize()
     return gh.wl.to_f64(gh.to_host(out, dt), dt)
 
@@ -171,23 +172,22 @@ ONE_WAVE_CASES = [c for c in ATTN_CASES if c[4] == 128 and c[6] == "bf16"][:6]
 
 @pytest.mark.parametrize("case", ONE_WAVE_CASES, ids=[f"P{c[0]}-N{c[1]}-G{c[2]}-Hkv{c[3]}-{c[5]}"
                                                       for c in ONE_WAVE_CASES])
-def test_attention_one_wave_kernel(case, monkeypatch):
+def test_attention_one_wave_kernel(case):
     """head_dim 128 has two kernels (two waves per row group splitting each
     key tile, the default, and one wave per row group); both match the
     oracle."""
     P, N, G, Hkv, D, kind, dt = case
     print(f"case attention one-wave kernel {case}", flush=True)
-    monkeypatch.setenv("OOO_ATTN_SPLITK", "0")
     rs, q, k, v, cap = _attn_inputs(P, N, G, Hkv, D, dt, seed=sum(case[:5]) + 1)
     t = _trie(kind, N, rs)
     mask = ov.ancestor_masks(t["parent"], (N + 63) // 64)
-    got = _run_attn(q, k, v, P, N, mask, G * Hkv, Hkv, D, dt)
+    got = _run_attn(q, k, v, P, N, mask, G * Hkv, Hkv, D, dt, variant=1)
     ref = ov.tree_attention(wl.to_f64(q, dt), wl.to_f64(k, dt), wl.to_f64(v, dt), P, t["parent"], Hkv)
     assert gh.row_rel_err(got, ref) <= gh.ATTN_TOL
 
 
-@pytest.mark.parametrize("splits", ["1", "3", "32"])
-def test_attention_split_counts_agree(splits, monkeypatch):
+@pytest.mark.parametrize("splits", [1, 3, 32])
+def test_attention_split_counts_agree(splits):
     """The split-KV decomposition does not change the result beyond rounding,
     and each setting is bitwise reproducible."""
     print(f"case attention splits={splits}", flush=True)
@@ -195,26 +195,25 @@ def test_attention_split_counts_agree(splits, monkeypatch):
     rs, q, k, v, cap = _attn_inputs(P, N, G, Hkv, D, "bf16", seed=7)
     t = _trie("random", N, rs)
     mask = ov.ancestor_masks(t["parent"], 1)
-    monkeypatch.setenv("OOO_ATTN_SPLITS", splits)
-    a = _run_attn(q, k, v, P, N, mask, G * Hkv, Hkv, D, "bf16")
-    b = _run_attn(q, k, v, P, N, mask, G * Hkv, Hkv, D, "bf16")
+    a = _run_attn(q, k, v, P, N, mask, G * Hkv, Hkv, D, "bf16", force_splits=splits)
+    b = _run_attn(q, k, v, P, N, mask, G * Hkv, Hkv, D, "bf16", force_splits=splits)
     assert np.array_equal(a, b)
     ref = ov.tree_attention(wl.to_f64(q, "bf16"), wl.to_f64(k, "bf16"), wl.to_f64(v, "bf16"), P, t["parent"], Hkv)
     assert gh.row_rel_err(a, ref) <= gh.ATTN_TOL
 
 
-def test_attention_workspace_reuse_across_shapes(monkeypatch):
+def test_attention_workspace_reuse_across_shapes():
     """One workspace serves calls of different shapes, head sizes and split
-    counts in a row: nothing a call reads from it is left over from another."""
+    counts in a row: nothing a call reads from it is left over from another
+    (the workspace starts out as NaN)."""
     print("case attention workspace reuse", flush=True)
-    shapes = [(1500, 64, 4, 2, 128, "16"), (300, 33, 2, 3, 64, "5"), (4096, 64, 4, 8, 128, "16"), (700, 100, 4, 1, 128, "7")]
+    shapes = [(1500, 64, 4, 2, 128, 16), (300, 33, 2, 3, 64, 5), (4096, 64, 4, 8, 128, 16), (700, 100, 4, 1, 128, 7),
+              (4096, 64, 4, 8, 128, 13)]
     need = 0
     for P, N, G, Hkv, D, splits in shapes:
-        monkeypatch.setenv("OOO_ATTN_SPLITS", splits)
-        need = max(need, ooo.tree_attn_workspace(N, G * Hkv, Hkv, D, P, ooo.BF16))
+        need = max(need, ooo.tree_attn_workspace(N, G * Hkv, Hkv, D, P, ooo.BF16, splits))
     ws = torch.full((need // 4 + 1,), float("nan"), dtype=torch.float32, device=DEV)
     for P, N, G, Hkv, D, splits in shapes:
-        monkeypatch.setenv("OOO_ATTN_SPLITS", splits)
         rs, q, k, v, cap = _attn_inputs(P, N, G, Hkv, D, "bf16", seed=P + N)
         t = _trie("random", N, rs)
         W = (N + 63) // 64
@@ -222,7 +221,7 @@ def test_attention_workspace_reuse_across_shapes(monkeypatch):
         qd, kd, vd = gh.to_dev(q, "bf16", DEV), gh.to_dev(k, "bf16", DEV), gh.to_dev(v, "bf16", DEV)
         md = torch.from_numpy(mask.view(np.int64)).to(DEV)
         out = torch.full((N, G * Hkv, D), float("nan"), dtype=torch.bfloat16, device=DEV)
-        ooo.tree_attn(qd, kd, vd, P, N, md, G * Hkv, Hkv, 1.0 / math.sqrt(D), out, ws)
+        ooo.tree_attn(qd, kd, vd, P, N, md, G * Hkv, Hkv, 1.0 / math.sqrt(D), out, ws, force_splits=splits)
         torch.cuda.synchronize()
         got = gh.wl.to_f64(gh.to_host(out, "bf16"), "bf16")
         ref = ov.tree_attention(wl.to_f64(q, "bf16"), wl.to_f64(k, "bf16"), wl.to_f64(v, "bf16"), P, t["parent"], Hkv)
