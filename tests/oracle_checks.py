@@ -438,6 +438,79 @@ def check_sequential_greedy(ov):
 
 
 # ----------------------------------------------------------------------------
+# the whole step on the tiny workload (Section 4.5, verify and commit)
+
+
+def _path_sdpa(q, k, v, P, parent, G):
+    """Each node's output by causal SDPA over [prefix; its root path]."""
+    N = len(parent)
+    out = np.empty_like(q)
+    for i in range(N):
+        chain = []
+        j = i
+        while j >= 0:
+            chain.append(j)
+            j = int(parent[j])
+        chain = chain[::-1]
+        rows = list(range(P)) + [P + a for a in chain]
+        allowed = np.ones((1, len(rows)), dtype=bool)
+        out[i] = _sdpa(q[i:i + 1], k[:, rows], v[:, rows], allowed, G)[0]
+    return out
+
+
+def check_verify_step(ov):
+    """The composed oracle step on the fp32 workload (two layers' draws) returns what
+    its inputs fix independently of it: the trie of brute-force prefix
+    enumeration; the greedy token each node's hidden row was built to select
+    (a margin wide enough that no other token competes); the planted
+    acceptance depth, the plant branch's nodes as the path, and the bonus the
+    deepest of them selects; and per-node attention equal to causal SDPA over
+    the prefix and the node's own root path."""
+    import sys
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    from paper_2608_00814_amd import workload as wl
+    cfg = wl.CONFIGS["tiny-fp32"]
+    for seed in range(2):
+        cands = wl.candidates_for(cfg, seed, 0)
+        token, parent, _, _ = brute_pack(cands.root_token, cands.seqs, cands.max_nodes, cands.max_depth)
+        token, parent = np.array(token), np.array(parent)
+        N = len(token)
+        tau, d = wl.designated_tokens(cfg, seed, 0, cands, token, parent)
+        w = wl.lm_head_weight(cfg, seed)
+        x = wl.to_f64(wl.hidden_rows(cfg, seed, 0, w, tau, N), cfg.dtype)
+        layers = []
+        for layer in range(2):  # two layers of the workload's draws, so a mix-up of layers shows
+            k, v = wl.layer_cache(cfg, seed, layer, N)
+            q = wl.queries(cfg, seed, 0, layer, N)
+            layers.append((wl.to_f64(q, cfg.dtype), wl.to_f64(k, cfg.dtype), wl.to_f64(v, cfg.dtype)))
+        res = ov.verify_step(cands.root_token, cands.seqs, cands.max_nodes, cands.max_depth, layers,
+                             cfg.prefix_len, cfg.n_kv_heads, x, wl.to_f64(w, cfg.dtype))
+        assert res["tree"]["token"].tolist() == token.tolist()
+        assert res["tree"]["parent"].tolist() == parent.tolist()
+        assert np.asarray(res["ids"]).tolist() == tau.tolist()
+        # the plant branch's first d tokens are nodes of the trie, in order
+        plant = cands.seqs[cands.plant_index]
+        index = {(): 0}
+        for i in range(1, N):
+            chain = []
+            j = i
+            while j > 0:
+                chain.append(int(token[j]))
+                j = int(parent[j])
+            index[tuple(chain[::-1])] = i
+        path = [index[tuple(plant[:kk])] for kk in range(d + 1)]
+        assert res["L"] == d
+        assert np.asarray(res["path"]).tolist()[: d + 1] == path
+        assert res["bonus"] == int(tau[path[-1]])
+        assert np.asarray(res["committed"]).tolist() == [int(t) for t in plant[:d]] + [int(tau[path[-1]])]
+        G = cfg.n_q_heads // cfg.n_kv_heads
+        assert len(res["attn"]) == len(layers)
+        for (ql, kl, vl), got in zip(layers, res["attn"]):
+            ref = _path_sdpa(ql, kl, vl, cfg.prefix_len, parent, G)
+            np.testing.assert_allclose(got, ref, rtol=1e-10, atol=1e-12)
+
+
+# ----------------------------------------------------------------------------
 # hint-bank continuations and lane filling (Section 4.4)
 
 
@@ -520,6 +593,7 @@ ALL_CHECKS = [
     check_compact_golden,
     check_compact_gather_scatter,
     check_sequential_greedy,
+    check_verify_step,
     check_hint_golden,
     check_hint_bruteforce,
 ]

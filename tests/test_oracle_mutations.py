@@ -45,6 +45,11 @@ MUTATIONS = [
     ("hint_one_token_too_many", "and len(cont) < max_len:", "and len(cont) <= max_len:"),
     ("lanes_native_first", "    lanes = [list(h) for h in hints][:n_lanes]\n    for c in native:",
      "    lanes = [list(h) for h in native][:n_lanes]\n    for c in hints:"),
+    ("step_accepts_on_own_tokens", "    acc = accept_walk(tree[\"token\"], tree[\"parent\"], greedy[\"ids\"])",
+     "    acc = accept_walk(tree[\"token\"], tree[\"parent\"], tree[\"token\"])"),
+    ("step_first_layer_only", "    outs = [tree_attention(q, k, v, prefix_len, tree[\"parent\"], n_kv_heads) for (q, k, v) in layers]",
+     "    outs = [tree_attention(q, layers[0][1], v, prefix_len, tree[\"parent\"], n_kv_heads) for (q, k, v) in layers]"),
+    ("step_logits_of_attention_input", "    logits = lm_head_logits(x, w)", "    logits = lm_head_logits(x[::-1], w)"),
     ("compact_dest_by_node", "    pairs = [(prefix_len + int(path[d]), prefix_len + d) for d in range(len(path))]",
      "    pairs = [(prefix_len + int(path[d]), prefix_len + int(path[d])) for d in range(len(path))]"),
 ]
