@@ -88,7 +88,7 @@ int ooo_version(void);
  *   cand_tokens     concatenated candidate continuations (after the root)
  *   cand_offsets    [n_cand + 1] CSR offsets into cand_tokens, in priority
  *                   order, non-decreasing, cand_offsets[0] == 0
- *   max_nodes       node budget (>= 1), including the root
+ *   max_nodes       node budget (1..1024), including the root
  *   max_depth       depth cap (>= 0); the root has depth 0
  *   token, parent, depth   [max_nodes] int32 outputs; parent[0] == -1
  *   anc_mask        [max_nodes * mask_words] uint64 output; bit j of row i is
@@ -100,8 +100,11 @@ int ooo_version(void);
  * parent[i] < i and siblings carry distinct tokens.  A token equal to an
  * existing child is shared; once the budget is full no node is added and the
  * rest of each candidate from its first unplaceable token is dropped.
+ * Host memory only; synchronous; keeps no state between calls and allocates
+ * nothing.
  * Errors: OOO_ERR_INVALID for null pointers, n_cand < 0, max_nodes < 1,
- * max_depth < 0, non-monotone offsets, negative tokens, or too few mask words.
+ * max_depth < 0, non-monotone offsets, negative tokens, or too few mask words;
+ * OOO_ERR_UNSUPPORTED for max_nodes > 1024 (the device kernels' limit).
  */
 int ooo_pack_tree(int32_t root_token, const int32_t* cand_tokens, const int32_t* cand_offsets,
                   int32_t n_cand, int32_t max_nodes, int32_t max_depth, int32_t* token,
@@ -269,21 +272,29 @@ int ooo_lmhead_argmax(const void* hidden, const void* weight, int32_t n_nodes,
  * DEVICE pointers.
  *   token, parent, depth, anc_mask   the packed trie (ooo_pack_tree layout)
  *   argmax_ids   [n_nodes] greedy token of every node
- *   path_cap     entries in `path`; must exceed the trie's deepest depth
+ *   max_depth    the deepest node depth the trie may hold (the max_depth it
+ *                was packed with)
+ *   path_cap     entries in `path`; at least max_depth + 1
  *   path         [path_cap] int32 out: path[d] = accepted node at depth d for
  *                d <= L, -1 beyond; path[0] == 0
  *   accept_len   [1] int32 out: L, the number of accepted draft nodes
  *   bonus_token  [1] int32 out: argmax_ids[path[L]]
  * The step commits token[path[1..L]] followed by the bonus token (L + 1
  * tokens).  Precondition (guaranteed by ooo_pack_tree): parent[i] < i and
- * siblings carry distinct tokens.
- * Errors: OOO_ERR_INVALID (null pointers, n_nodes < 1, path_cap < 1,
- * 64 * mask_words < n_nodes, mask_words > 16), OOO_ERR_HIP.
+ * siblings carry distinct tokens.  A trie whose accepted path runs deeper
+ * than path_cap - 1 (deeper than the max_depth it was declared with) is
+ * reported on the device, not shortened: accept_len = -1, bonus_token = -1
+ * and path all -1, and ooo_kv_compact then moves no row.
+ * Errors: OOO_ERR_INVALID (null pointers, n_nodes < 1, max_depth < 0,
+ * path_cap < 1, 64 * mask_words < n_nodes, mask_words > 16),
+ * OOO_ERR_CAPACITY (path_cap < max_depth + 1), OOO_ERR_HIP.
+ * Relative to the plain signature of this step, path_cap is an addition (the
+ * size of `path`, checked against max_depth).
  */
 int ooo_accept(const int32_t* token, const int32_t* parent, const int32_t* depth,
                const uint64_t* anc_mask, int32_t mask_words, const int32_t* argmax_ids,
-               int32_t n_nodes, int32_t path_cap, int32_t* path, int32_t* accept_len,
-               int32_t* bonus_token, void* stream);
+               int32_t n_nodes, int32_t max_depth, int32_t path_cap, int32_t* path,
+               int32_t* accept_len, int32_t* bonus_token, void* stream);
 
 /*
  * ooo_kv_compact - commit the accepted states (Section 4.5: only states on
@@ -307,7 +318,8 @@ int ooo_accept(const int32_t* token, const int32_t* parent, const int32_t* depth
  * handled (every source is read before its row can be overwritten).
  * Precondition: path is strictly increasing (true for any root path of a
  * packed trie).  Entries with path[d] >= n_nodes or L >= path_cap are
- * ignored on the device rather than read out of bounds.
+ * ignored on the device rather than read out of bounds; accept_len = -1
+ * (ooo_accept's report of a path deeper than path_cap - 1) moves no row.
  * Errors: OOO_ERR_INVALID (null pointers, sizes < 1, prefix_len < 0,
  * prefix_len + n_nodes > cap), OOO_ERR_UNSUPPORTED (head_dim * element size
  * not a multiple of 16 bytes), OOO_ERR_HIP.

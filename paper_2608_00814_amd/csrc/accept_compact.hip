@@ -66,17 +66,21 @@ __global__ __launch_bounds__(1024) void accept_kernel(const int32_t* __restrict_
 #pragma unroll
     for (int w = 0; w < kMaxMaskWords; ++w)
       if (w < W) ok = ok && ((am[w] & ~match[w]) == 0);
-    if (ok && dp < path_cap && dp < kMaxNodes) {
-      path_s[dp] = i;
+    if (ok) {
+      if (dp < path_cap && dp < kMaxNodes) path_s[dp] = i;
       atomicMax(&best_depth, dp);
     }
   }
   __syncthreads();
-  for (int k = tid; k < path_cap; k += blockDim.x) path[k] = k < kMaxNodes ? path_s[k] : -1;
+  // An accepted node deeper than path[] holds (a trie deeper than the
+  // caller's max_depth) is reported as accept_len = -1 with an empty path:
+  // the step commits nothing rather than a shortened path.
+  const bool overflow = best_depth >= path_cap || best_depth >= kMaxNodes;
+  for (int k = tid; k < path_cap; k += blockDim.x) path[k] = (!overflow && k < kMaxNodes) ? path_s[k] : -1;
   if (tid == 0) {
     const int L = best_depth;
-    *accept_len = L;
-    *bonus = ids_s[path_s[L]];
+    *accept_len = overflow ? -1 : L;
+    *bonus = overflow ? -1 : ids_s[path_s[L]];
   }
 }
 
@@ -99,7 +103,7 @@ __global__ __launch_bounds__(256) void kv_compact_kernel(uint8_t* __restrict__ k
     const int d = 1 + item / chunks;
     first_src[i] = (item < rows_per_pass * chunks && d < path_cap && d < N) ? path[d] : -1;
   }
-  int L = *accept_len;
+  int L = *accept_len;  // -1 (overflow reported by ooo_accept): nothing to move
   if (L > path_cap - 1) L = path_cap - 1;
   if (P_dev) P = min(max(*P_dev, 0), P);  // device prefix, bounded by the launch value
   for (int d0 = 1; d0 <= L; d0 += rows_per_pass) {
@@ -135,12 +139,15 @@ using namespace ooo;
 
 extern "C" int ooo_accept(const int32_t* token, const int32_t* parent, const int32_t* depth,
                           const uint64_t* anc_mask, int32_t mask_words, const int32_t* argmax_ids,
-                          int32_t n_nodes, int32_t path_cap, int32_t* path, int32_t* accept_len,
-                          int32_t* bonus_token, void* stream) {
+                          int32_t n_nodes, int32_t max_depth, int32_t path_cap, int32_t* path,
+                          int32_t* accept_len, int32_t* bonus_token, void* stream) {
   OOO_REQUIRE(token && parent && depth && anc_mask && argmax_ids && path && accept_len && bonus_token,
               OOO_ERR_INVALID, "ooo_accept: null pointer");
   OOO_REQUIRE(n_nodes >= 1, OOO_ERR_INVALID, "ooo_accept: n_nodes must be >= 1");
-  OOO_REQUIRE(path_cap >= 1, OOO_ERR_INVALID, "ooo_accept: path_cap must be >= 1");
+  OOO_REQUIRE(max_depth >= 0 && path_cap >= 1, OOO_ERR_INVALID,
+              "ooo_accept: max_depth (%d) must be >= 0 and path_cap (%d) >= 1", max_depth, path_cap);
+  OOO_REQUIRE(path_cap >= max_depth + 1, OOO_ERR_CAPACITY,
+              "ooo_accept: path of %d entries cannot hold a root path of depth %d", path_cap, max_depth);
   OOO_REQUIRE(mask_words >= 1 && mask_words <= kMaxMaskWords && (int64_t)mask_words * 64 >= n_nodes,
               OOO_ERR_INVALID, "ooo_accept: mask_words=%d cannot describe %d nodes (max %d words)", mask_words,
               n_nodes, kMaxMaskWords);

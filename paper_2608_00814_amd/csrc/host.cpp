@@ -31,11 +31,13 @@ extern "C" int ooo_version(void) { return OOO_ABI_VERSION; }
 // Candidate trie (Section 3, ToolSpec loop; Section 4.4, fixed candidate
 // budget with hint lanes first; Section 4.5, one candidate tree).  Children
 // are found by walking the parent's child list (first child, next sibling),
-// kept in per-thread buffers reused across calls; a trie has at most a few
-// hundred nodes, so the scan is short and the call allocates nothing once
-// warm.  The ancestor bitmask of a node is its parent's mask plus its own
-// bit, which is valid because a parent is always created before its
-// children.
+// kept in stack arrays bounded by the 1024-node limit of the device kernels
+// (the ancestor masks of the attention and accept kernels hold at most 16
+// words), so the call keeps no state and allocates nothing.  The ancestor
+// bitmask of a node is its parent's mask plus its own bit, which is valid
+// because a parent is always created before its children.
+constexpr int32_t kMaxTrieNodes = 1024;
+
 extern "C" int ooo_pack_tree(int32_t root_token, const int32_t* cand_tokens,
                              const int32_t* cand_offsets, int32_t n_cand, int32_t max_nodes,
                              int32_t max_depth, int32_t* token, int32_t* parent, int32_t* depth,
@@ -47,6 +49,8 @@ extern "C" int ooo_pack_tree(int32_t root_token, const int32_t* cand_tokens,
     OOO_REQUIRE(token && parent && depth && anc_mask && n_nodes && n_truncated, OOO_ERR_INVALID,
                 "an output pointer is null");
     OOO_REQUIRE(max_nodes >= 1, OOO_ERR_INVALID, "max_nodes must be >= 1 (got %d)", max_nodes);
+    OOO_REQUIRE(max_nodes <= kMaxTrieNodes, OOO_ERR_UNSUPPORTED, "max_nodes %d exceeds %d", max_nodes,
+                kMaxTrieNodes);
     OOO_REQUIRE(max_depth >= 0, OOO_ERR_INVALID, "max_depth must be >= 0 (got %d)", max_depth);
     OOO_REQUIRE(mask_words >= 1 && (int64_t)mask_words * 64 >= max_nodes, OOO_ERR_INVALID,
                 "mask_words=%d cannot hold %d nodes", mask_words, max_nodes);
@@ -60,11 +64,7 @@ extern "C" int ooo_pack_tree(int32_t root_token, const int32_t* cand_tokens,
     for (int32_t t = 0; t < total; ++t)
       OOO_REQUIRE(cand_tokens[t] >= 0, OOO_ERR_INVALID, "negative token at position %d", t);
 
-    thread_local std::vector<int32_t> first_child, next_sibling;
-    if (first_child.size() < (size_t)max_nodes) {
-      first_child.resize(max_nodes);
-      next_sibling.resize(max_nodes);
-    }
+    int32_t first_child[kMaxTrieNodes], next_sibling[kMaxTrieNodes];
     first_child[0] = -1;
     int32_t n = 1;
     int32_t dropped = 0;

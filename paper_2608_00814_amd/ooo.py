@@ -48,7 +48,7 @@ SIGNATURES = {
     "ooo_lmhead_pack": (ctypes.c_int, [_vp, _i32, _i32, ctypes.c_int, _vp, _sz, _vp]),
     "ooo_lmhead_argmax": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, ctypes.c_int, _i32, _vp, _vp, _vp, _vp, _sz,
                                          _vp]),
-    "ooo_accept": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i32, _vp, _i32, _i32, _vp, _vp, _vp, _vp]),
+    "ooo_accept": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i32, _vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp]),
     "ooo_kv_compact": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i64, _i32, ctypes.c_int, _i32, _vp, _i32, _vp, _vp,
                                       _i32, _vp]),
     "ooo_embed_rows": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _vp, _vp]),
@@ -335,16 +335,19 @@ def lmhead_argmax(hidden, weight, argmax_ids, max_logit, logits=None, workspace=
 
 
 def accept(token, parent, depth, anc_mask, argmax_ids, n_nodes: int, path, accept_len, bonus_token,
-           stream=None) -> None:
-    """All device int32 tensors (anc_mask int64 [N][W]); path [path_cap]."""
+           stream=None, max_depth: Optional[int] = None) -> None:
+    """All device int32 tensors (anc_mask int64 [N][W]); path [path_cap];
+    ``max_depth`` defaults to path_cap - 1.  accept_len comes back -1 when
+    the accepted path runs deeper than path_cap - 1 (nothing committed)."""
     for t, nm in ((token, "token"), (parent, "parent"), (depth, "depth"), (anc_mask, "anc_mask"),
                   (argmax_ids, "argmax_ids"), (path, "path"), (accept_len, "accept_len"),
                   (bonus_token, "bonus_token")):
         _dev(t, nm)
     W = anc_mask.shape[-1]
+    md = path.numel() - 1 if max_depth is None else max_depth
     _check(lib().ooo_accept(token.data_ptr(), parent.data_ptr(), depth.data_ptr(), anc_mask.data_ptr(), W,
-                            argmax_ids.data_ptr(), n_nodes, path.numel(), path.data_ptr(), accept_len.data_ptr(),
-                            bonus_token.data_ptr(), _stream(stream)))
+                            argmax_ids.data_ptr(), n_nodes, md, path.numel(), path.data_ptr(),
+                            accept_len.data_ptr(), bonus_token.data_ptr(), _stream(stream)))
 
 
 def kv_compact(k_cache, v_cache, prefix_len: int, n_nodes: int, path, accept_len, stream=None,

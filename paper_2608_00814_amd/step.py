@@ -131,7 +131,7 @@ class VerifyRunner:
     def accept(self, stream=None) -> None:
         N = self.n_nodes
         ooo.accept(self.token[:N], self.parent[:N], self.depth[:N], self.mask[:N], self.ids[:N], N, self.path,
-                   self.accept_len, self.bonus, stream)
+                   self.accept_len, self.bonus, stream, max_depth=self.max_depth)
 
     def compact(self, k_cache, v_cache, prefix_len: int, stream=None, prefix_dev=None) -> None:
         ooo.kv_compact(k_cache, v_cache, prefix_len, self.n_nodes, self.path, self.accept_len, stream,
@@ -143,6 +143,9 @@ class VerifyRunner:
     def result(self) -> StepResult:
         r = self.h_res.numpy()
         L = int(r[0])
+        if L < 0:
+            raise ooo.OooError(ooo.ERR_CAPACITY, f"accepted path deeper than max_depth {self.max_depth}: "
+                               "nothing was committed")
         return StepResult(self.n_nodes, self.n_truncated, L, int(r[1]), r[2:2 + L + 1].copy())
 
     def set_weight(self, weight, packed: Optional[bool] = None) -> None:

@@ -144,6 +144,20 @@ def test_pack_rejects_bad_arguments(kwargs):
     assert ooo.last_error() != ""
 
 
+def test_pack_node_limit_and_no_state_between_calls():
+    """The 1024-node limit of the device kernels is reported; a full-size
+    pack after a small one (and the reverse) gives the reference trie each
+    time: nothing carries over between calls."""
+    assert _call_pack(max_nodes=1025, W=17) == ooo.ERR_UNSUPPORTED
+    assert "exceeds 1024" in ooo.last_error()
+    rs = np.random.default_rng(21)
+    big = [[int(t) for t in rs.integers(0, 3, size=int(rs.integers(1, 30)))] for _ in range(200)]
+    small = [[5, 6], [5, 7]]
+    for cands, nodes in [(big, 1024), (small, 8), (big, 1024), (small, 3)]:
+        r, ref = _pack_both(2, cands, nodes, 64)
+        _assert_same(r, ref)
+
+
 def test_layer_entry_points_validate_on_host():
     L = ooo.lib()
     fake = ctypes.c_void_p(256)  # never dereferenced: every call below fails validation first
@@ -210,7 +224,7 @@ def test_device_entry_points_validate_on_host():
     assert "null" in ooo.last_error()
     assert L.ooo_lmhead_argmax(fake, None, 4, 64, 100, ooo.BF16, ooo.W_ROWS, fake, fake, None, fake, 1 << 20, None) \
         == ooo.ERR_INVALID
-    assert L.ooo_accept(fake, fake, fake, fake, 1, fake, 4, 8, None, fake, fake, None) == ooo.ERR_INVALID
+    assert L.ooo_accept(fake, fake, fake, fake, 1, fake, 4, 7, 8, None, fake, fake, None) == ooo.ERR_INVALID
     assert L.ooo_kv_compact(fake, fake, 2, 2, 100, 64, ooo.BF16, 10, None, 4, None, fake, 8, None) == ooo.ERR_INVALID
     # inconsistent shapes
     assert L.ooo_tree_attn(fake, fake, fake, 100, 97, None, 4, fake, 1, 4, 1, 64, 0.1, ooo.BF16, fake, None, 0, None) \
@@ -221,8 +235,12 @@ def test_device_entry_points_validate_on_host():
         == ooo.ERR_INVALID  # too few mask words
     assert L.ooo_tree_attn(fake, fake, fake, 100, 10, None, 0, fake, 1, 4, 1, 64, 0.1, ooo.BF16, fake, None, 0, None) \
         == ooo.ERR_INVALID
-    assert L.ooo_accept(fake, fake, fake, fake, 1, fake, 65, 8, fake, fake, fake, None) == ooo.ERR_INVALID
-    assert L.ooo_accept(fake, fake, fake, fake, 1, fake, 4, 0, fake, fake, fake, None) == ooo.ERR_INVALID
+    assert L.ooo_accept(fake, fake, fake, fake, 1, fake, 65, 7, 8, fake, fake, fake, None) == ooo.ERR_INVALID
+    assert L.ooo_accept(fake, fake, fake, fake, 1, fake, 4, 0, 0, fake, fake, fake, None) == ooo.ERR_INVALID
+    assert L.ooo_accept(fake, fake, fake, fake, 1, fake, 4, -1, 8, fake, fake, fake, None) == ooo.ERR_INVALID
+    # a path buffer that cannot hold a root path of the declared depth
+    assert L.ooo_accept(fake, fake, fake, fake, 1, fake, 4, 8, 8, fake, fake, fake, None) == ooo.ERR_CAPACITY
+    assert "cannot hold" in ooo.last_error()
     assert L.ooo_kv_compact(fake, fake, 2, 2, 100, 64, ooo.BF16, 97, None, 4, fake, fake, 8, None) == ooo.ERR_INVALID
     # unsupported but valid
     assert L.ooo_tree_attn(fake, fake, fake, 100, 10, None, 4, fake, 1, 4, 1, 96, 0.1, ooo.BF16, fake, None, 0, None) \

@@ -403,6 +403,41 @@ def test_accept_planted(N, kind, target):
     assert np.array_equal(p[:d + 1], ref["path"]) and np.all(p[d + 1:] == -1)
 
 
+@pytest.mark.parametrize("planted", [3, 10])
+def test_accept_reports_a_path_deeper_than_declared(planted):
+    """A chain of depth 10 verified with a path buffer of 5 entries (declared
+    max_depth 4): an accepted path that fits is returned as usual; one that
+    runs deeper is reported (accept_len -1, path all -1) rather than
+    shortened, and compaction then moves no row."""
+    print(f"case accept overflow planted={planted}", flush=True)
+    N = 11
+    rs = np.random.default_rng(5)
+    t = _trie("chain", N, rs)
+    token = t["token"]
+    ids = np.full(N, 10 ** 6, np.int32)
+    for k in range(planted):
+        ids[k] = token[k + 1]
+    tok_d, par_d, dep_d, mask_d = _upload_trie(t, 1)
+    ids_d = torch.from_numpy(ids).to(DEV)
+    pth = torch.full((5,), 99, dtype=torch.int32, device=DEV)
+    L = torch.full((1,), -5, dtype=torch.int32, device=DEV)
+    bonus = torch.full((1,), -5, dtype=torch.int32, device=DEV)
+    ooo.accept(tok_d, par_d, dep_d, mask_d, ids_d, N, pth, L, bonus, max_depth=4)
+    P, Hkv, D = 7, 2, 64
+    cache = torch.randn(2, 1, Hkv, P + N + 1, D, device=DEV).to(torch.bfloat16)
+    before = cache.clone()
+    ooo.kv_compact(cache[0], cache[1], P, N, pth, L)
+    torch.cuda.synchronize()
+    if planted <= 4:
+        ref = ov.accept_walk(token, t["parent"], ids)
+        assert int(L.item()) == ref["L"] == planted and int(bonus.item()) == ref["bonus"]
+        assert pth.cpu().numpy()[:planted + 1].tolist() == list(range(planted + 1))
+    else:
+        assert int(L.item()) == -1 and int(bonus.item()) == -1
+        assert (pth.cpu().numpy() == -1).all()
+        assert torch.equal(cache, before)
+
+
 @pytest.mark.parametrize("dt", ["bf16", "f32"])
 @pytest.mark.parametrize("path", [[0], [0, 2, 3], [0, 1, 5, 6], [0, 1, 2, 3, 4], list(range(0, 130, 2)),
                                   [0, 9, 10, 11, 40, 41, 63]])
