@@ -60,3 +60,40 @@ def test_source_digest_ignores_comments_and_layout(tmp_path, monkeypatch, path):
     (tmp_path / "c.hip").write_text(text + "\nint x;\n")
     assert bench._source_digest("a.hip") == bench._source_digest("b.hip")
     assert bench._source_digest("a.hip") != bench._source_digest("c.hip")
+
+
+def test_step_time_statistics():
+    st = bench.step_time_stats([0.001 * k for k in range(1, 101)])  # 1..100 ms
+    assert st["median_ms"] == pytest.approx(50.5)
+    assert st["p10_ms"] == pytest.approx(10.9)
+    assert st["p90_ms"] == pytest.approx(90.1)
+
+
+def test_host_cpu_reports_model_and_affinity():
+    model, cores = bench.host_cpu()
+    assert isinstance(model, str) and model
+    assert cores == len(os.sched_getaffinity(0)) >= 1
+    if os.path.exists("/proc/cpuinfo"):
+        first = next(l for l in open("/proc/cpuinfo") if l.startswith("model name"))
+        assert model == first.split(":", 1)[1].strip()
+
+
+def test_paper_context_and_mat_tokens():
+    # the paper's mean accepted tokens per call for Qwen3-8B on API-Bank (Table 2)
+    assert bench.PAPER_MAT_QWEN3_8B == 8.35
+    t = bench.tokens_at_mat(1000.0)
+    assert t["tokens_per_s"] == 8350.0 and t["mean_accepted_tokens_per_call"] == 8.35
+    ctx = bench.PAPER_CONTEXT
+    assert ctx["speedup_over_autoregressive"].startswith("2.46x-5.34x")
+    assert "H100" in ctx["hardware"] and "Table 2" in ctx["source"]
+    assert ctx["qwen3_8b_api_bank"]["speedup"] == 5.34
+
+
+def test_cpu_baseline_uses_every_core_of_the_affinity():
+    """The oracle's BLAS pool is limited to the process affinity (not left at
+    whatever size the pool happened to start with)."""
+    threadpoolctl = pytest.importorskip("threadpoolctl")
+    cores = len(os.sched_getaffinity(0))
+    with bench._blas_limit(cores):
+        sizes = [i.get("num_threads") for i in threadpoolctl.threadpool_info() if i.get("user_api") == "blas"]
+    assert all(n == cores for n in sizes)
