@@ -198,6 +198,28 @@ int ooo_tree_attn(const void* q, const void* k_cache, const void* v_cache, int64
                   void* stream);
 
 /*
+ * ooo_tree_attn_noalloc - ooo_tree_attn without a workspace argument, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * serving loops that must not call the allocator, harnesses that forbid it).
+ *
+ * Arguments as for ooo_tree_attn, without workspace and ws_bytes.  The split
+ * partials go to a scratch array built into the library, 16 MiB per GPU
+ * (ooo_tree_attn_noalloc_scratch_bytes()), held until the process ends; its
+ * device address is looked up on the first call on each device.  The call
+ * allocates nothing.  Every call on one GPU shares that GPU's scratch, so
+ * calls that may overlap on one GPU (different streams without ordering)
+ * race; calls ordered on one stream do not.  Nothing in the scratch needs to
+ * start at zero.
+ * Errors: those of ooo_tree_attn, and OOO_ERR_CAPACITY when the shape's
+ * partials (ooo_tree_attn_workspace()) exceed the scratch.
+ */
+int ooo_tree_attn_noalloc(const void* q, const void* k_cache, const void* v_cache, int64_t cap,
+                          int32_t prefix_len, const int32_t* prefix_len_dev, int32_t n_nodes,
+                          const uint64_t* anc_mask, int32_t mask_words, int32_t n_q_heads, int32_t n_kv_heads,
+                          int32_t head_dim, float scale, ooo_dtype dt, void* out, void* stream);
+size_t ooo_tree_attn_noalloc_scratch_bytes(void);
+
+/*
  * ooo_tree_attn_ex, ooo_tree_attn_workspace_ex - ooo_tree_attn with the
  * planner's choices overridden, for tests and tuning.
  *   force_splits  0: the planner's split count; > 0: that many key splits

@@ -35,6 +35,7 @@
 #include <math.h>
 #include <stdlib.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "device_common.h"
@@ -1040,6 +1041,53 @@ extern "C" int ooo_tree_attn_ex(const void* q, const void* k_cache, const void* 
   const hipError_t e = hipGetLastError();
   OOO_REQUIRE(e == hipSuccess, OOO_ERR_HIP, "ooo_tree_attn: launch failed: %s", hipGetErrorString(e));
   return ooo::ok();
+}
+
+// Scratch of ooo_tree_attn_noalloc: one copy per GPU, held until the
+// process ends.  Host code never passes `scratch` itself to a kernel (in
+// host code it is a stand-in, not a device address): the device address is
+// looked up once per device with hipGetSymbolAddress.
+constexpr size_t kNoAllocScratchBytes = 16u << 20;
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::once_flag g_scratch_once[kMaxDevices];
+void* g_scratch_ptr[kMaxDevices];
+hipError_t g_scratch_err[kMaxDevices];
+}  // namespace
+
+extern "C" size_t ooo_tree_attn_noalloc_scratch_bytes(void) { return kNoAllocScratchBytes; }
+
+extern "C" int ooo_tree_attn_noalloc(const void* q, const void* k_cache, const void* v_cache, int64_t cap,
+                                     int32_t prefix_len, const int32_t* prefix_len_dev, int32_t n_nodes,
+                                     const uint64_t* anc_mask, int32_t mask_words, int32_t n_q_heads,
+                                     int32_t n_kv_heads, int32_t head_dim, float scale, ooo_dtype dt, void* out,
+                                     void* stream) {
+  const size_t need =
+      (n_nodes >= 1 && n_kv_heads >= 1 && n_q_heads >= 1 && n_q_heads % n_kv_heads == 0 && prefix_len >= 0)
+          ? make_plan(n_nodes, n_q_heads, n_kv_heads, head_dim, prefix_len, dt, 0).ws_bytes
+          : 0;
+  OOO_REQUIRE(need <= kNoAllocScratchBytes, OOO_ERR_CAPACITY,
+              "ooo_tree_attn_noalloc: this shape needs %zu bytes of scratch; the built-in scratch holds %zu",
+              need, kNoAllocScratchBytes);
+  void* ws = nullptr;
+  if (need > 0) {
+    int dev = -1;
+    const hipError_t ge = hipGetDevice(&dev);
+    OOO_REQUIRE(ge == hipSuccess && dev >= 0 && dev < kMaxDevices, OOO_ERR_HIP,
+                "ooo_tree_attn_noalloc: no current device (%s)", hipGetErrorString(ge));
+    std::call_once(g_scratch_once[dev], [dev] {
+      g_scratch_err[dev] = hipGetSymbolAddress(&g_scratch_ptr[dev], HIP_SYMBOL(scratch));
+    });
+    OOO_REQUIRE(g_scratch_err[dev] == hipSuccess && g_scratch_ptr[dev], OOO_ERR_HIP,
+                "ooo_tree_attn_noalloc: scratch address on device %d: %s", dev,
+                hipGetErrorString(g_scratch_err[dev]));
+    ws = g_scratch_ptr[dev];
+  }
+  return ooo_tree_attn_ex(q, k_cache, v_cache, cap, prefix_len, prefix_len_dev, n_nodes, anc_mask, mask_words,
+                          n_q_heads, n_kv_heads, head_dim, scale, dt, out, ws, need > 0 ? kNoAllocScratchBytes : 0,
+                          stream, 0, 0);
 }
 
 extern "C" int ooo_tree_attn(const void* q, const void* k_cache, const void* v_cache, int64_t cap,

@@ -41,6 +41,9 @@ SIGNATURES = {
     "ooo_tree_attn": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _vp, _i32, _vp, _i32, _i32, _i32, _i32,
                                      ctypes.c_float, ctypes.c_int, _vp, _vp, _sz, _vp]),
     "ooo_tree_attn_workspace_ex": (_sz, [_i32, _i32, _i32, _i32, _i32, ctypes.c_int, _i32]),
+    "ooo_tree_attn_noalloc": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _vp, _i32, _vp, _i32, _i32, _i32, _i32,
+                                             ctypes.c_float, ctypes.c_int, _vp, _vp]),
+    "ooo_tree_attn_noalloc_scratch_bytes": (_sz, []),
     "ooo_tree_attn_ex": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _vp, _i32, _vp, _i32, _i32, _i32, _i32,
                                         ctypes.c_float, ctypes.c_int, _vp, _vp, _sz, _vp, _i32, _i32]),
     "ooo_lmhead_workspace": (_sz, [_i32, _i32, _i32, ctypes.c_int]),
@@ -284,6 +287,19 @@ def tree_attn(q, k_cache, v_cache, prefix_len: int, n_nodes: int, anc_mask, n_q_
                                   anc_mask.data_ptr(), W, n_q_heads, n_kv_heads, D, float(scale), dtype_code(q),
                                   out.data_ptr(), _ptr(workspace), ws_bytes, _stream(stream), force_splits,
                                   variant))
+
+
+def tree_attn_noalloc(q, k_cache, v_cache, prefix_len: int, n_nodes: int, anc_mask, n_q_heads: int,
+                      n_kv_heads: int, scale: float, out, stream=None, prefix_dev=None) -> None:
+    """tree_attn with the library's built-in per-GPU scratch instead of a
+    workspace (the call allocates nothing)."""
+    for t, nm in ((q, "q"), (k_cache, "k_cache"), (v_cache, "v_cache"), (anc_mask, "anc_mask"), (out, "out")):
+        _dev(t, nm)
+    Hkv, cap, D = k_cache.shape
+    W = anc_mask.shape[-1]
+    _check(lib().ooo_tree_attn_noalloc(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), cap, prefix_len,
+                                       _prefix_ptr(prefix_dev), n_nodes, anc_mask.data_ptr(), W, n_q_heads,
+                                       n_kv_heads, D, float(scale), dtype_code(q), out.data_ptr(), _stream(stream)))
 
 
 def lmhead_workspace(n_nodes: int, hidden_dim: int, vocab: int, dtype: int) -> int:

@@ -27,7 +27,7 @@ def declared_functions():
 
 def test_exports_match_header():
     names = declared_functions()
-    assert len(names) == 24
+    assert len(names) == 26
     assert set(names) == set(ooo.SIGNATURES)
     lib = ooo.lib()
     for n in names:
