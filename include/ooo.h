@@ -396,7 +396,9 @@ int ooo_rmsnorm(const float* h, const void* weight, int32_t n_rows, int32_t dim,
  *            rows (out_dim = 2 I, I % 128 == 0) and out [n_rows][I] bf16 gets
  *            silu(gate) * up.  out must not alias x or weight.
  *   workspace, ws_bytes   ooo_linear_workspace(n_rows, in_dim, out_dim)
- *            bytes of partial sums
+ *            bytes of partial sums (fp16 times a power of two per 32 output
+ *            columns, so a float32 output carries a relative rounding error
+ *            of about 2^-11 per partial sum; they are added in float32)
  * Deterministic: partial sums are added in a fixed order (no atomics).
  * Errors: OOO_ERR_INVALID (null pointers, sizes < 1, unknown layout or
  * epilogue), OOO_ERR_UNSUPPORTED (in_dim % 64, n_rows > 256, SwiGLU with

@@ -15,11 +15,14 @@
 //  * Inside a block: two loader waves DMA the W chunk (two 32-row slots
 //    each) and a third the X chunk into a 6-stage LDS ring; four compute
 //    waves run mfma_f32_32x32x16_bf16 (32 W rows x the nodes each).
-//  * At the end of each tile segment a block stores its partial sums (fp32,
-//    [node][128 rows]) in the workspace; a reduce kernel adds a tile's
-//    partials in block order (deterministic, no atomics) and applies the
-//    epilogue: store fp32 or bf16, add into an fp32 output (the residual
-//    rows), or silu(gate) * up of a fused gate/up projection.
+//  * At the end of each tile segment a block stores its partial sums in the
+//    workspace as fp16 ([node][128 rows]) times a power of two per compute
+//    wave (its 32 rows), chosen so that the wave's largest magnitude lies
+//    in [2^14, 2^15): half the bytes of fp32, with the range of fp32.  A
+//    reduce kernel adds a tile's partials in float32 in block order
+//    (deterministic, no atomics) and applies the epilogue: store fp32 or
+//    bf16, add into an fp32 output (the residual rows), or silu(gate) * up
+//    of a fused gate/up projection.
 #include <math.h>
 
 #include <vector>
@@ -43,6 +46,14 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 
 constexpr int kRows = 128;  // W rows per tile (4 compute waves x 32)
+
+// Stream-K partial sums in the workspace: slot k (block b, segment j: k =
+// b * seg + j) holds v[k][node][128 rows] in fp16 and sc[k][4], the factor
+// that turns the fp16 values of rows 32 w .. 32 w + 31 back into the sums.
+struct Partials {
+  uint16_t* v;
+  float* sc;
+};
 
 template <int NB>
 struct Ring {
@@ -75,7 +86,7 @@ __host__ __device__ __forceinline__ long long run_lo(long long C, int b, int B) 
 template <int NB, bool PACKED>
 __global__ __launch_bounds__(448) void linear_bf16_kernel(const uint16_t* __restrict__ X,
                                                           const uint16_t* __restrict__ Wt, int N, int K, int O,
-                                                          int seg_per_block, float* __restrict__ part) {
+                                                          int seg_per_block, Partials part) {
   using R = Ring<NB>;
   constexpr int NPAD = 32 * NB;
   __shared__ __attribute__((aligned(1024))) uint8_t lds[R::BYTES];
@@ -174,14 +185,29 @@ __global__ __launch_bounds__(448) void linear_bf16_kernel(const uint16_t* __rest
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) acc[nb] = mfma32(af[s4], bf[nb][s4], acc[nb]);
     if (q == total - 1 || kc == KC - 1) {
-      // segment done: acc[nb][j] = partial of tile row wave*32 + 8(j/4) + 4u + j%4, node 32nb + c
-      float* dst = part + ((size_t)b * seg_per_block + (t - first_tile)) * NPAD * kRows;
+      // segment done: acc[nb][j] = partial of tile row wave*32 + 8(j/4) + 4u + j%4, node 32nb + c.
+      // Scale: the wave's largest magnitude a < 2^ex goes to [2^14, 2^15)
+      // (fp16 holds up to 65504); exact powers of two both ways.  Inf and
+      // NaN stay what they are.
+      float amax = 0.f;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) amax = __builtin_fmaxf(amax, __builtin_fabsf(acc[nb][j]));
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) amax = __builtin_fmaxf(amax, shfl_xor_f(amax, o));
+      const int ex = min(max(__builtin_amdgcn_frexp_expf(amax), -100), 100);
+      const float mul = __builtin_amdgcn_ldexpf(1.f, 15 - ex);
+      const size_t slot = (size_t)b * seg_per_block + (t - first_tile);
+      uint16_t* dst = part.v + slot * NPAD * kRows;
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
         for (int jq = 0; jq < 4; ++jq)
-          *reinterpret_cast<f32x4*>(dst + (size_t)(32 * nb + c) * kRows + wave * 32 + 8 * jq + 4 * u) =
-              f32x4{acc[nb][4 * jq], acc[nb][4 * jq + 1], acc[nb][4 * jq + 2], acc[nb][4 * jq + 3]};
+          *reinterpret_cast<u32x2*>(dst + (size_t)(32 * nb + c) * kRows + wave * 32 + 8 * jq + 4 * u) =
+              u32x2{pack_f16x2(acc[nb][4 * jq] * mul, acc[nb][4 * jq + 1] * mul),
+                    pack_f16x2(acc[nb][4 * jq + 2] * mul, acc[nb][4 * jq + 3] * mul)};
+      if (lane == 0) part.sc[slot * 4 + wave] = __builtin_amdgcn_ldexpf(1.f, ex - 15);
     }
   }
 }
@@ -219,29 +245,49 @@ __device__ int tile_slots(long long C, int B, int KC, int seg, int t, int* slots
   return n;
 }
 
-// Four blocks per output tile (per gate tile for kSwiGLU), 32 rows each;
-// thread item (n, 4 consecutive rows), so partial reads are 16 bytes and
-// contiguous across threads.  Partials are added in block order; the slot
-// loop is unrolled so that its loads are in flight together.
-__device__ __forceinline__ f32x4 slot_sum(const float* __restrict__ part, const int* slots, int ns, size_t stride,
-                                          size_t e) {
-  f32x4 s = {0.f, 0.f, 0.f, 0.f};
-  int i = 0;
-  for (; i + 4 <= ns; i += 4) {
-    const f32x4 a = *reinterpret_cast<const f32x4*>(part + slots[i] * stride + e);
-    const f32x4 b = *reinterpret_cast<const f32x4*>(part + slots[i + 1] * stride + e);
-    const f32x4 c = *reinterpret_cast<const f32x4*>(part + slots[i + 2] * stride + e);
-    const f32x4 d = *reinterpret_cast<const f32x4*>(part + slots[i + 3] * stride + e);
-    s += a;
-    s += b;
-    s += c;
-    s += d;
+// Sum of the partials at element e (node n, tile row r: e = n * 128 + r)
+// over a tile's slot list (from tile_slots), in block order whichever
+// kernel adds them (the same rounding).  The loads of a batch of S slots
+// (S = 4, 8 or 16, the smallest that holds the list; longer lists take
+// several batches) are all issued before the first add, so a sum costs one
+// round trip to memory rather than one per four slots; slots past the end of
+// the list re-read the last one and are not added.
+// fp16 partial values at element e of slot k: 4 (f32x4) or 1 (float)
+__device__ __forceinline__ void load_part(const Partials& p, int k, size_t stride, size_t e, f32x4& x, float& sc) {
+  const u32x2 h = *reinterpret_cast<const u32x2*>(p.v + k * stride + e);
+  const f32x2_t lo = unpack_f16x2(h[0]), hi = unpack_f16x2(h[1]);
+  x = f32x4{lo[0], lo[1], hi[0], hi[1]};
+  sc = p.sc[k * 4 + (int)(e % kRows) / 32];
+}
+__device__ __forceinline__ void load_part(const Partials& p, int k, size_t stride, size_t e, float& x, float& sc) {
+  x = unpack_f16x2(p.v[k * stride + e])[0];
+  sc = p.sc[k * 4 + (int)(e % kRows) / 32];
+}
+template <typename T, int S>
+__device__ __forceinline__ T slot_batches(const Partials& part, const int* slots, int ns, size_t stride, size_t e) {
+  T s{};
+  for (int i0 = 0; i0 < ns; i0 += S) {
+    T x[S];
+    float sc[S];
+#pragma unroll
+    for (int i = 0; i < S; ++i) load_part(part, slots[min(i0 + i, ns - 1)], stride, e, x[i], sc[i]);
+#pragma unroll
+    for (int i = 0; i < S; ++i)
+      if (i0 + i < ns) s += x[i] * sc[i];
   }
-  for (; i < ns; ++i) s += *reinterpret_cast<const f32x4*>(part + slots[i] * stride + e);
   return s;
 }
+template <typename T>
+__device__ __forceinline__ T slot_sum_of(const Partials& part, const int* slots, int ns, size_t stride, size_t e) {
+  if (ns <= 4) return slot_batches<T, 4>(part, slots, ns, stride, e);
+  if (ns <= 8) return slot_batches<T, 8>(part, slots, ns, stride, e);
+  return slot_batches<T, 16>(part, slots, ns, stride, e);
+}
 
-__global__ __launch_bounds__(256) void linear_reduce_kernel(const float* __restrict__ part, int N, int npad, int K,
+// Four blocks per output tile (per gate tile for kSwiGLU), 32 rows each;
+// thread item (n, 4 consecutive rows), so partial reads are 16 bytes and
+// contiguous across threads.
+__global__ __launch_bounds__(256) void linear_reduce_kernel(Partials part, int N, int npad, int K,
                                                             int O, int B, int seg, int epi, void* __restrict__ out,
                                                             int inter) {
   __shared__ int slots[2][256];
@@ -259,9 +305,9 @@ __global__ __launch_bounds__(256) void linear_reduce_kernel(const float* __restr
     const int n = item >> 3, r = quarter * 32 + 4 * (item & 7);
     const size_t e = (size_t)n * kRows + r;
     const int col = t * kRows + r;
-    const f32x4 sv = slot_sum(part, slots[0], ns0, stride, e);
+    const f32x4 sv = slot_sum_of<f32x4>(part, slots[0], ns0, stride, e);
     if (epi == kSwiGLU) {
-      const f32x4 uv = slot_sum(part, slots[1], ns1, stride, e);
+      const f32x4 uv = slot_sum_of<f32x4>(part, slots[1], ns1, stride, e);
       uint16_t* o = reinterpret_cast<uint16_t*>(out) + (size_t)n * inter + col;
 #pragma unroll
       for (int j = 0; j < 4; ++j)
@@ -279,28 +325,6 @@ __global__ __launch_bounds__(256) void linear_reduce_kernel(const float* __restr
   }
 }
 
-// Sum of the partials at element e (node n, tile row r: e = n * 128 + r)
-// over a tile's slot list (from tile_slots), in block order as the reduce
-// kernel adds them (same rounding); loads issued four at a time.
-template <typename T>
-__device__ __forceinline__ T slot_sum_of(const float* __restrict__ part, const int* slots, int ns, size_t stride,
-                                         size_t e) {
-  T s{};
-  int i = 0;
-  for (; i + 4 <= ns; i += 4) {
-    const T x0 = *reinterpret_cast<const T*>(part + slots[i] * stride + e);
-    const T x1 = *reinterpret_cast<const T*>(part + slots[i + 1] * stride + e);
-    const T x2 = *reinterpret_cast<const T*>(part + slots[i + 2] * stride + e);
-    const T x3 = *reinterpret_cast<const T*>(part + slots[i + 3] * stride + e);
-    s += x0;
-    s += x1;
-    s += x2;
-    s += x3;
-  }
-  for (; i < ns; ++i) s += *reinterpret_cast<const T*>(part + slots[i] * stride + e);
-  return s;
-}
-
 // Slot-list capacity of the fused epilogues (checked on the host).
 constexpr int kMaxTileSlots = 64;
 constexpr int kMaxFusedTiles = 64;
@@ -310,7 +334,7 @@ constexpr int kMaxFusedTiles = 64;
 // sqrt(mean(h[n]^2) + eps) * w).  One block of 512 threads per row, four
 // float4 columns per thread (out_dim <= 8192).
 constexpr int kAddNormItems = 4;
-__global__ __launch_bounds__(512) void linear_add_rmsnorm_kernel(const float* __restrict__ part, int npad, int K,
+__global__ __launch_bounds__(512) void linear_add_rmsnorm_kernel(Partials part, int npad, int K,
                                                                  int O, int B, int seg, float* __restrict__ resid,
                                                                  const uint16_t* __restrict__ w, float eps,
                                                                  uint16_t* __restrict__ out) {
@@ -368,7 +392,7 @@ __global__ __launch_bounds__(512) void linear_add_rmsnorm_kernel(const float* __
 // P + n.
 template <int D>
 __global__ __launch_bounds__(1024) void linear_qk_norm_rope_kernel(
-    const float* __restrict__ part, int npad, int K, int B, int seg, const uint16_t* __restrict__ q_norm,
+    Partials part, int npad, int K, int B, int seg, const uint16_t* __restrict__ q_norm,
     const uint16_t* __restrict__ k_norm, float eps, const int32_t* __restrict__ depth, int P,
     const int32_t* __restrict__ P_dev, RopeFreq fr, int Hq, int Hkv, uint16_t* __restrict__ q_out,
     uint16_t* __restrict__ k_cache, uint16_t* __restrict__ v_cache, long long cap) {
@@ -416,8 +440,13 @@ __global__ __launch_bounds__(1024) void linear_qk_norm_rope_kernel(
 
 struct LinPlan {
   int nb, blocks, seg;
+  size_t val_bytes;  // fp16 partial values (the factors follow)
   size_t ws_bytes;
 };
+
+Partials partials_in(void* workspace, const LinPlan& p) {
+  return Partials{(uint16_t*)workspace, (float*)((uint8_t*)workspace + p.val_bytes)};
+}
 
 LinPlan lin_plan(int N, int K, int O) {
   LinPlan p{};
@@ -427,7 +456,8 @@ LinPlan lin_plan(int N, int K, int O) {
   p.blocks = (int)(C < cus ? C : cus);
   const long long run = (C + p.blocks - 1) / p.blocks;
   p.seg = (int)(run / (K / 64)) + 2;  // tiles a run can touch
-  p.ws_bytes = (size_t)p.blocks * p.seg * (32 * p.nb) * kRows * sizeof(float);
+  p.val_bytes = ((size_t)p.blocks * p.seg * (32 * p.nb) * kRows * sizeof(uint16_t) + 255) / 256 * 256;
+  p.ws_bytes = p.val_bytes + (size_t)p.blocks * p.seg * 4 * sizeof(float);
   return p;
 }
 
@@ -483,7 +513,7 @@ static int stream_k(const char* who, const void* x, const void* weight, int32_t 
               who, p.ws_bytes, ws_bytes);
   const uint16_t* X = (const uint16_t*)x;
   const uint16_t* W = (const uint16_t*)weight;
-  float* part = (float*)workspace;
+  const Partials part = partials_in(workspace, p);
   const bool pk = weight_layout == OOO_W_PACKED;
 #define OOO_LIN_LAUNCH(NBV)                                                                                        \
   do {                                                                                                            \
@@ -513,7 +543,7 @@ extern "C" int ooo_linear(const void* x, const void* weight, int32_t n_rows, int
   LinPlan p{};
   const int rc = stream_k("ooo_linear", x, weight, n_rows, in_dim, out_dim, weight_layout, workspace, ws_bytes, st, &p);
   if (rc != OOO_OK) return rc;
-  float* part = (float*)workspace;
+  const Partials part = partials_in(workspace, p);
   const int tiles = (out_dim + kRows - 1) / kRows;
   const int rgrid = 4 * (epilogue == OOO_EPI_SWIGLU_BF16 ? tiles / 2 : tiles);
   linear_reduce_kernel<<<rgrid, 256, 0, st>>>(part, n_rows, 32 * p.nb, in_dim, out_dim, p.blocks, p.seg, (int)epilogue,
@@ -541,7 +571,7 @@ extern "C" int ooo_linear_add_rmsnorm(const void* x, const void* weight, int32_t
   const int rc = stream_k("ooo_linear_add_rmsnorm", x, weight, n_rows, in_dim, out_dim, weight_layout, workspace,
                           ws_bytes, st, &p);
   if (rc != OOO_OK) return rc;
-  linear_add_rmsnorm_kernel<<<n_rows, 512, 0, st>>>((const float*)workspace, 32 * p.nb, in_dim, out_dim, p.blocks,
+  linear_add_rmsnorm_kernel<<<n_rows, 512, 0, st>>>(partials_in(workspace, p), 32 * p.nb, in_dim, out_dim, p.blocks,
                                                      p.seg, residual, (const uint16_t*)norm_weight, eps,
                                                      (uint16_t*)normed_out);
   const hipError_t e = hipGetLastError();
@@ -578,7 +608,7 @@ extern "C" int ooo_linear_qk_norm_rope(const void* x, const void* weight, int32_
   if (rc != OOO_OK) return rc;
   const RopeFreq fr = rope_freq(rope_theta, head_dim);
   const dim3 grid(n_rows, (nh + 15) / 16);
-  const float* part = (const float*)workspace;
+  const Partials part = partials_in(workspace, p);
   if (head_dim == 128)
     linear_qk_norm_rope_kernel<128><<<grid, 1024, 0, st>>>(part, 32 * p.nb, in_dim, p.blocks, p.seg,
                                                             (const uint16_t*)q_norm, (const uint16_t*)k_norm, eps, depth,

@@ -28,6 +28,13 @@ from paper_2608_00814_amd.model import ModelRunner
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
 TOL = gh.ATTN_TOL
+# fp32 outputs of the streaming projection: the stream-K partial sums pass
+# through the workspace as fp16 (times a power of two per 32 rows), so each
+# partial element carries a relative rounding error of at most 2^-11; over a
+# row the error is at most 2^-11 * ||sum_s |p_s| || / ||sum_s p_s||, which is
+# about 2^-11 * sqrt(S) for S independent partials (S <= 16 slots per tile
+# at these shapes): 2e-3.  Measured: 3.6e-4 at N=64, K=4096, O=6144.
+F32_OUT_TOL = 2e-3
 f64 = wl.bf16_to_f64
 
 
@@ -71,7 +78,7 @@ def test_linear(N, K, O, packed):
     ws = torch.zeros(ooo.linear_workspace(N, K, O), dtype=torch.uint8, device=DEV)
     y32 = torch.full((N, O), float("nan"), dtype=torch.float32, device=DEV)
     ooo.linear(xd, wl_, y32, ooo.EPI_STORE_F32, ws)
-    assert gh.row_rel_err(y32.double().cpu().numpy(), ref) <= 1e-4
+    assert gh.row_rel_err(y32.double().cpu().numpy(), ref) <= F32_OUT_TOL
     again = torch.empty_like(y32)
     ooo.linear(xd, wl_, again, ooo.EPI_STORE_F32, ws)
     assert torch.equal(y32, again)
@@ -81,7 +88,7 @@ def test_linear(N, K, O, packed):
     base = rs.normal(size=(N, O)).astype(np.float32)
     acc = torch.from_numpy(base).to(DEV)
     ooo.linear(xd, wl_, acc, ooo.EPI_ADD_F32, ws)
-    assert gh.row_rel_err(acc.double().cpu().numpy(), ref + base) <= 1e-4
+    assert gh.row_rel_err(acc.double().cpu().numpy(), ref + base) <= F32_OUT_TOL
     if O % 256 == 0:
         I = O // 2
         act = torch.empty(N, I, dtype=torch.bfloat16, device=DEV)
@@ -111,7 +118,7 @@ def test_linear_add_rmsnorm(N, K, O):
     torch.cuda.synchronize()
     assert torch.equal(h_fused, h_ref)
     ref_h = base.astype(np.float64) + f64(x) @ f64(w).T
-    assert gh.row_rel_err(h_fused.double().cpu().numpy(), ref_h) <= 1e-4
+    assert gh.row_rel_err(h_fused.double().cpu().numpy(), ref_h) <= F32_OUT_TOL
     assert gh.row_rel_err(_host_f64(out), om.rmsnorm(h_fused.double().cpu().numpy(), f64(nw), 1e-6)) <= TOL
 
 
