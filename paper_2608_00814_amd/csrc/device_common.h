@@ -24,6 +24,23 @@ constexpr int kWave = 64;
 // streaming 13.9 GB per step does not see).
 constexpr int kStreamOnce = 2;
 
+// Address-space casts for the LDS-DMA builtin (global source, LDS target).
+#define OOO_LDS(p) ((__attribute__((address_space(3))) void*)(p))
+#define OOO_GLB(p) ((const __attribute__((address_space(1))) void*)(p))
+
+// Workgroup barrier without the memory-model fence __syncthreads() adds.
+// The LDS DMA (global_load_lds) is invisible to the compiler's waits, so a
+// kernel waits for its own DMA explicitly (wait_vmcnt) before the barrier;
+// the "memory" clobber keeps the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// s_waitcnt vmcnt(N) (N <= 63), leaving the other counters alone.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x0F70);
+}
+
 __device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) {
   return __uint_as_float(static_cast<uint32_t>(b) << 16);
 }

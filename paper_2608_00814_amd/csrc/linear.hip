@@ -12,9 +12,10 @@
 //    contiguous run of chunks [C b / B, C (b + 1) / B).  Every block streams
 //    the same number of bytes whatever O and K are; a run covers the end of
 //    one tile and the start of the next.
-//  * Inside a block: two loader waves DMA the W chunk (two 32-row slots
-//    each) and a third the X chunk into a 6-stage LDS ring; four compute
-//    waves run mfma_f32_32x32x16_bf16 (32 W rows x the nodes each).
+//  * Inside a block, the LM head's streaming core (stream_core.h): two
+//    loader waves DMA the W chunk (two 32-row slots each) and a third the X
+//    chunk into an LDS ring; four compute waves run mfma_f32_32x32x16_bf16
+//    (32 W rows x the nodes each).
 //  * At the end of each tile segment a block stores its partial sums in the
 //    workspace as fp16 ([node][128 rows]) times a power of two per compute
 //    wave (its 32 rows), chosen so that the wave's largest magnitude lies
@@ -30,22 +31,12 @@
 #include "device_common.h"
 #include "ooo_internal.h"
 #include "rope.h"
+#include "stream_core.h"
 
 namespace ooo {
 namespace {
 
-#define OOO_LDS(p) ((__attribute__((address_space(3))) void*)(p))
-#define OOO_GLB(p) ((const __attribute__((address_space(1))) void*)(p))
-
-__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
-
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x0F70);
-}
-
-constexpr int kRows = 128;  // W rows per tile (4 compute waves x 32)
+constexpr int kRows = kStreamRows;  // W rows per tile (4 compute waves x 32)
 
 // Stream-K partial sums in the workspace: slot k (block b, segment j: k =
 // b * seg + j) holds v[k][node][128 rows] in fp16 and sc[k][4], the factor
@@ -55,39 +46,14 @@ struct Partials {
   float* sc;
 };
 
-template <int NB>
-struct Ring {
-  static constexpr int XR = 32 * NB;        // node rows staged (padded)
-  static constexpr int WS = kRows * 128;    // bytes of a W chunk
-  static constexpr int XS = XR * 128;       // bytes of an X chunk
-  static constexpr int NS = NB == 1 ? 7 : NB == 2 ? 6 : NB == 4 ? 4 : 3;
-  static constexpr int XREG = NS * WS;
-  static constexpr int BYTES = NS * (WS + XS);
-  static constexpr int WDMA = WS / 1024 / 2;  // DMA instructions per W chunk and W loader
-  static constexpr int XDMA = XS / 1024;
-  static_assert((NS - 2) * WDMA <= 63 && (NS - 2) * XDMA <= 63, "vmcnt range");
-  static_assert(BYTES <= 160 * 1024, "LDS capacity");
-};
-
-template <int PER, int MAXA>
-__device__ __forceinline__ void wait_chunks(int ahead) {
-  static_assert(MAXA <= 5, "ring depth");
-  if (MAXA >= 5 && ahead >= 5) wait_vmcnt<(MAXA >= 5 ? 5 * PER : 0)>();
-  else if (MAXA >= 4 && ahead == 4) wait_vmcnt<(MAXA >= 4 ? 4 * PER : 0)>();
-  else if (MAXA >= 3 && ahead == 3) wait_vmcnt<(MAXA >= 3 ? 3 * PER : 0)>();
-  else if (MAXA >= 2 && ahead == 2) wait_vmcnt<(MAXA >= 2 ? 2 * PER : 0)>();
-  else if (ahead == 1) wait_vmcnt<PER>();
-  else wait_vmcnt<0>();
-}
-
 // first chunk of block b's run
 __host__ __device__ __forceinline__ long long run_lo(long long C, int b, int B) { return C * b / B; }
 
 template <int NB, bool PACKED>
-__global__ __launch_bounds__(448) void linear_bf16_kernel(const uint16_t* __restrict__ X,
+__global__ __launch_bounds__(kStreamThreads) void linear_bf16_kernel(const uint16_t* __restrict__ X,
                                                           const uint16_t* __restrict__ Wt, int N, int K, int O,
                                                           int seg_per_block, Partials part) {
-  using R = Ring<NB>;
+  using R = StreamRing<NB>;
   constexpr int NPAD = 32 * NB;
   __shared__ __attribute__((aligned(1024))) uint8_t lds[R::BYTES];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -112,51 +78,29 @@ __global__ __launch_bounds__(448) void linear_bf16_kernel(const uint16_t* __rest
         ++it;
       }
       if (!is_x) {
+        // this loader's slots 2 half, 2 half + 1: tile rows 64 half .. +63
         uint8_t* dst = lds + stage * R::WS + half * (R::WS / 2);
-        if (PACKED) {
-          const uint16_t* src = Wt + ((size_t)t * KC + kc) * (kRows * 64) + half * (kRows * 32) + lane * 8;
 #pragma unroll
-          for (int j = 0; j < R::WDMA; ++j)
-            __builtin_amdgcn_global_load_lds(OOO_GLB(src + j * 512), OOO_LDS(dst + j * 1024), 16, 0,
-                                             kStreamOnce);
-        } else {
-#pragma unroll
-          for (int j = 0; j < R::WDMA; ++j) {
-            const int r = half * 64 + 8 * j + lane / 8;  // tile row; lane = (row, physical piece)
-            const int pc = (lane % 8) ^ (r % 8);
-            const int row = min(t * kRows + r, O - 1);
-            __builtin_amdgcn_global_load_lds(OOO_GLB(Wt + (size_t)row * K + kc * 64 + pc * 8),
-                                             OOO_LDS(dst + j * 1024), 16, 0, kStreamOnce);
-          }
+        for (int sl = 0; sl < 2; ++sl) {
+          const int s4 = 2 * half + sl;
+          if (PACKED)
+            dma_w_slot_packed(Wt + (((size_t)t * KC + kc) * kRows + 32 * s4) * 64 + lane * 8, 1, dst + sl * 4096);
+          else
+            dma_w_slot_rows(Wt, K, t * kRows + 32 * s4, O, kc, dst + sl * 4096, lane);
         }
       } else {
-        uint8_t* dst = lds + R::XREG + stage * R::XS;
-#pragma unroll
-        for (int j = 0; j < R::XDMA; ++j) {
-          const int r = 8 * j + lane / 8;
-          const int pc = (lane % 8) ^ (r % 8);
-          const int row = min(r, N - 1);
-          __builtin_amdgcn_global_load_lds(OOO_GLB(X + (size_t)row * K + kc * 64 + pc * 8),
-                                           OOO_LDS(dst + j * 1024), 16, 0, 0);
-        }
+        dma_x_chunk<NB>(X, N, K, kc, lds + R::XREG + stage * R::XS, lane);
       }
     };
-    for (int q = 0; q < R::NS - 1 && q < total; ++q) issue(q, q);
-    for (int q = 0; q < total; ++q) {
-      const int ahead = min(R::NS - 2, total - 1 - q);
-      if (is_x) wait_chunks<R::XDMA, R::NS - 2>(ahead);
-      else wait_chunks<R::WDMA, R::NS - 2>(ahead);
-      wg_barrier();
-      if (q + R::NS - 1 < total) issue(q + R::NS - 1, (q + R::NS - 1) % R::NS);
-    }
+    if (is_x) loader_stream<R::NS, R::XDMA>(total, issue);
+    else loader_stream<R::NS, R::WDMA>(total, issue);
     return;
   }
 
   // ------------------------------------------------------------------ compute
   const int c = lane & 31, u = lane >> 5;
-  uint32_t off[4];  // piece 2s+u of row c, swizzled
-#pragma unroll
-  for (int s4 = 0; s4 < 4; ++s4) off[s4] = c * 128 + (((2 * s4 + u) ^ (c % 8)) << 4);
+  uint32_t off[4];
+  frag_offsets(lane, off);
   const uint32_t wrow = wave * 32 * 128;
   f32x16 acc[NB];
   int t = first_tile, kc = (int)(lo - (long long)first_tile * KC) - 1;
@@ -171,19 +115,7 @@ __global__ __launch_bounds__(448) void linear_bf16_kernel(const uint16_t* __rest
     }
     const int stage = q % R::NS;
     wg_barrier();
-    const uint8_t* Ws = lds + stage * R::WS + wrow;
-    const uint8_t* Xs = lds + R::XREG + stage * R::XS;
-    bf16x8 af[4], bf[NB][4];
-#pragma unroll
-    for (int s4 = 0; s4 < 4; ++s4) {
-      af[s4] = as_bf16x8(*reinterpret_cast<const u32x4*>(Ws + off[s4]));
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) bf[nb][s4] = as_bf16x8(*reinterpret_cast<const u32x4*>(Xs + nb * 4096 + off[s4]));
-    }
-#pragma unroll
-    for (int s4 = 0; s4 < 4; ++s4)
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) acc[nb] = mfma32(af[s4], bf[nb][s4], acc[nb]);
+    chunk_mfma<NB>(lds + stage * R::WS + wrow, lds + R::XREG + stage * R::XS, off, acc);
     if (q == total - 1 || kc == KC - 1) {
       // segment done: acc[nb][j] = partial of tile row wave*32 + 8(j/4) + 4u + j%4, node 32nb + c.
       // Scale: the wave's largest magnitude a < 2^ex goes to [2^14, 2^15)
@@ -518,9 +450,9 @@ static int stream_k(const char* who, const void* x, const void* weight, int32_t 
 #define OOO_LIN_LAUNCH(NBV)                                                                                        \
   do {                                                                                                            \
     if (pk)                                                                                                       \
-      linear_bf16_kernel<NBV, true><<<p.blocks, 448, 0, st>>>(X, W, n_rows, in_dim, out_dim, p.seg, part);         \
+      linear_bf16_kernel<NBV, true><<<p.blocks, kStreamThreads, 0, st>>>(X, W, n_rows, in_dim, out_dim, p.seg, part);         \
     else                                                                                                          \
-      linear_bf16_kernel<NBV, false><<<p.blocks, 448, 0, st>>>(X, W, n_rows, in_dim, out_dim, p.seg, part);        \
+      linear_bf16_kernel<NBV, false><<<p.blocks, kStreamThreads, 0, st>>>(X, W, n_rows, in_dim, out_dim, p.seg, part);        \
   } while (0)
   if (p.nb == 1) OOO_LIN_LAUNCH(1);
   else if (p.nb == 2) OOO_LIN_LAUNCH(2);

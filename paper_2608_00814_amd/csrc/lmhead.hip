@@ -10,14 +10,11 @@
 //    wave), so that no block streams more than one group beyond the average
 //    (1187 tiles on 256 blocks: 4 tiles + 2 or 3 groups each, instead of 4
 //    or 5 tiles).
-//  * Two loader waves copy each chunk of W (128 rows x 128 B) and of X
-//    (all nodes x 128 B) from global memory straight into a 3-5 stage LDS
-//    ring with global_load_lds: every DMA instruction moves 8 whole rows.
-//    The 16-byte pieces of a row are XOR-swizzled by (row % 8).
-//  * Four compute waves own 32 rows each and read A (W) and B (X) MFMA
-//    fragments from LDS; they never issue global loads in the loop.
-//  * The contraction index inside a chunk follows the pieces: MFMA k-step s,
-//    lane half u, element e is k = 8 * (2s + u) + e for both operands.
+//  * The streaming core (stream_core.h): two loader waves copy each W
+//    chunk (128 rows x 128 B) and a third the X chunk (all nodes x 128 B)
+//    straight into an LDS ring with global_load_lds; four compute waves own
+//    32 rows each and run the MFMAs from LDS, never issuing global loads in
+//    the loop.
 //  * Each lane ends a tile with 16 logits of one node; the per-node argmax is
 //    kept in registers across tiles, merged across the block's waves in LDS
 //    and across blocks by a small finalize kernel (value, then lowest index).
@@ -25,6 +22,7 @@
 
 #include "device_common.h"
 #include "ooo_internal.h"
+#include "stream_core.h"
 
 namespace ooo {
 namespace {
@@ -34,54 +32,14 @@ struct Cand {
   int i;
 };
 
-typedef short i16x4_t __attribute__((ext_vector_type(4)));
-#define OOO_LDS(p) ((__attribute__((address_space(3))) void*)(p))
-#define OOO_GLB(p) ((const __attribute__((address_space(1))) void*)(p))
-
-__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
-
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x0F70);
-}
-
-constexpr int kLmRows = 128;  // vocabulary rows per tile (4 waves x 32)
-
-// Ring of NS stages; NS - 2 chunks are in flight while one is consumed.
-// Wider node tiles need more X bytes per stage, so fewer stages fit.  Two
-// loader waves split each W chunk (two 32-row slots each), a third loads X.
-template <int NB>
-struct LmRing {
-  static constexpr int XR = 32 * NB;            // node rows staged (padded)
-  static constexpr int WS = kLmRows * 128;      // bytes of a W chunk
-  static constexpr int XS = XR * 128;           // bytes of an X chunk
-  static constexpr int NS = NB == 1 ? 7 : NB == 2 ? 6 : NB == 4 ? 4 : 3;
-  static constexpr int XREG = NS * WS;          // start of the X stages
-  static constexpr int BYTES = NS * (WS + XS);
-  static constexpr int WDMA = WS / 1024 / 2;    // DMA instructions per W chunk and W loader
-  static constexpr int XDMA = XS / 1024;
-  static_assert((NS - 2) * WDMA <= 63 && (NS - 2) * XDMA <= 63, "vmcnt range");
-  static_assert(BYTES + 4 * 32 * NB * 8 <= 160 * 1024, "LDS capacity");
-};
-
-// wait until at most `ahead` chunks of `per` DMA instructions are pending
-template <int PER, int MAXA>
-__device__ __forceinline__ void wait_chunks(int ahead) {
-  static_assert(MAXA <= 5, "ring depth");
-  if (MAXA >= 5 && ahead >= 5) wait_vmcnt<(MAXA >= 5 ? 5 * PER : 0)>();
-  else if (MAXA >= 4 && ahead == 4) wait_vmcnt<(MAXA >= 4 ? 4 * PER : 0)>();
-  else if (MAXA >= 3 && ahead == 3) wait_vmcnt<(MAXA >= 3 ? 3 * PER : 0)>();
-  else if (MAXA >= 2 && ahead == 2) wait_vmcnt<(MAXA >= 2 ? 2 * PER : 0)>();
-  else if (ahead == 1) wait_vmcnt<PER>();
-  else wait_vmcnt<0>();
-}
+constexpr int kLmRows = kStreamRows;  // vocabulary rows per tile (4 waves x 32)
 
 template <int NB, bool PACKED>
-__global__ __launch_bounds__(448) void lmhead_bf16_kernel(const uint16_t* __restrict__ X,
+__global__ __launch_bounds__(kStreamThreads) void lmhead_bf16_kernel(const uint16_t* __restrict__ X,
                                                           const uint16_t* __restrict__ Wt, int N, int H, int V,
                                                           Cand* __restrict__ partial, float* __restrict__ logits) {
-  using R = LmRing<NB>;
+  using R = StreamRing<NB>;
+  static_assert(R::BYTES + 4 * 32 * NB * sizeof(Cand) <= 160 * 1024, "LDS capacity");
   __shared__ __attribute__((aligned(1024))) uint8_t lds[R::BYTES];
   __shared__ Cand red[4][32 * NB];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -136,57 +94,30 @@ __global__ __launch_bounds__(448) void lmhead_bf16_kernel(const uint16_t* __rest
       if (!is_x) {
         uint8_t* dst = lds + stage * R::WS;
         if (t != issue_tile) set_tile(t);
-        // DMA instruction j fills rows 8j .. 8j+7 of the stage: slot j / 4
+        // slot s4's 32 rows go to LDS rows 32 s4 .. 32 s4 + 31 of the stage
 #pragma unroll
         for (int s4 = 0; s4 < 4; ++s4) {
           if (s4 / 2 != s_lo / 2) continue;
-          const uint16_t* src = sbase[s4] + kc * sstep[s4];
           if (PACKED || sstep[s4] == 0) {
-#pragma unroll
-            for (int jj = 0; jj < 4; ++jj)
-              __builtin_amdgcn_global_load_lds(OOO_GLB(src + (sstep[s4] ? jj * 512 : 0)),
-                                               OOO_LDS(dst + (4 * s4 + jj) * 1024), 16, 0, kStreamOnce);
+            dma_w_slot_packed(sbase[s4] + kc * sstep[s4], sstep[s4], dst + s4 * 4096);
           } else {
-            const int gi = group_of(t, s4);
-#pragma unroll
-            for (int jj = 0; jj < 4; ++jj) {
-              const int r = 8 * jj + lane / 8;  // group row; lane = (row, physical piece)
-              const int pc = (lane % 8) ^ (r % 8);
-              const int row = min(32 * gi + r, V - 1);
-              __builtin_amdgcn_global_load_lds(OOO_GLB(Wt + (size_t)row * H + kc * 64 + pc * 8),
-                                               OOO_LDS(dst + (4 * s4 + jj) * 1024), 16, 0, kStreamOnce);
-            }
+            dma_w_slot_rows(Wt, H, 32 * group_of(t, s4), V, kc, dst + s4 * 4096, lane);
           }
         }
       } else {
-        uint8_t* dst = lds + R::XREG + stage * R::XS;
-#pragma unroll
-        for (int j = 0; j < R::XDMA; ++j) {
-          const int r = 8 * j + lane / 8;
-          const int pc = (lane % 8) ^ (r % 8);
-          const int row = min(r, N - 1);
-          __builtin_amdgcn_global_load_lds(OOO_GLB(X + (size_t)row * H + kc * 64 + pc * 8),
-                                           OOO_LDS(dst + j * 1024), 16, 0, 0);
-        }
+        dma_x_chunk<NB>(X, N, H, kc, lds + R::XREG + stage * R::XS, lane);
       }
     };
-    for (int q = 0; q < R::NS - 1 && q < total; ++q) issue(q, q);
-    for (int q = 0; q < total; ++q) {
-      const int ahead = min(R::NS - 2, total - 1 - q);  // chunks issued after q
-      if (is_x) wait_chunks<R::XDMA, R::NS - 2>(ahead);
-      else wait_chunks<R::WDMA, R::NS - 2>(ahead);
-      wg_barrier();
-      if (q + R::NS - 1 < total) issue(q + R::NS - 1, (q + R::NS - 1) % R::NS);
-    }
+    if (is_x) loader_stream<R::NS, R::XDMA>(total, issue);
+    else loader_stream<R::NS, R::WDMA>(total, issue);
     __syncthreads();  // matches the compute waves' final reduction barrier
     return;
   }
 
   // ------------------------------------------------------------------ compute
   const int c = lane & 31, u = lane >> 5;
-  uint32_t off[4];  // piece 2s+u of row c, swizzled
-#pragma unroll
-  for (int s4 = 0; s4 < 4; ++s4) off[s4] = c * 128 + (((2 * s4 + u) ^ (c % 8)) << 4);
+  uint32_t off[4];
+  frag_offsets(lane, off);
   const uint32_t wrow = wave * 32 * 128;
 
   float bestv[NB];
@@ -208,19 +139,7 @@ __global__ __launch_bounds__(448) void lmhead_bf16_kernel(const uint16_t* __rest
     const int stage = q % R::NS;
     wg_barrier();
     if (gi < 0) continue;  // empty slot of the last round (barriers only)
-    const uint8_t* Ws = lds + stage * R::WS + wrow;
-    const uint8_t* Xs = lds + R::XREG + stage * R::XS;
-    bf16x8 af[4], bf[NB][4];
-#pragma unroll
-    for (int s4 = 0; s4 < 4; ++s4) {
-      af[s4] = as_bf16x8(*reinterpret_cast<const u32x4*>(Ws + off[s4]));
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) bf[nb][s4] = as_bf16x8(*reinterpret_cast<const u32x4*>(Xs + nb * 4096 + off[s4]));
-    }
-#pragma unroll
-    for (int s4 = 0; s4 < 4; ++s4)
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) acc[nb] = mfma32(af[s4], bf[nb][s4], acc[nb]);
+    chunk_mfma<NB>(lds + stage * R::WS + wrow, lds + R::XREG + stage * R::XS, off, acc);
 
     if (kc == chunks - 1) {
       // tile done: acc[nb][j] = logit of vocabulary row v0 + 8(j/4) + 4u + j%4, node 32nb + c
@@ -425,9 +344,9 @@ extern "C" int ooo_lmhead_argmax(const void* hidden, const void* weight, int32_t
 #define OOO_LM_LAUNCH(NBV)                                                                                   \
   do {                                                                                                      \
     if (pk)                                                                                                 \
-      lmhead_bf16_kernel<NBV, true><<<p.blocks, 448, 0, st>>>(X, W, n_nodes, hidden_dim, vocab, part, logits); \
+      lmhead_bf16_kernel<NBV, true><<<p.blocks, kStreamThreads, 0, st>>>(X, W, n_nodes, hidden_dim, vocab, part, logits); \
     else                                                                                                    \
-      lmhead_bf16_kernel<NBV, false><<<p.blocks, 448, 0, st>>>(X, W, n_nodes, hidden_dim, vocab, part, logits); \
+      lmhead_bf16_kernel<NBV, false><<<p.blocks, kStreamThreads, 0, st>>>(X, W, n_nodes, hidden_dim, vocab, part, logits); \
   } while (0)
     if (p.nb == 1) OOO_LM_LAUNCH(1);
     else if (p.nb == 2) OOO_LM_LAUNCH(2);

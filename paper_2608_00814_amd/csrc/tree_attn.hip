@@ -70,18 +70,10 @@ struct AttnArgs {
 __device__ __forceinline__ int sigma(int c) { return (c & ~0xC) | ((c & 4) << 1) | ((c & 8) >> 1); }
 
 typedef short i16x4 __attribute__((ext_vector_type(4)));
-#define OOO_LDS(p) ((__attribute__((address_space(3))) void*)(p))
-#define OOO_GLB(p) ((const __attribute__((address_space(1))) void*)(p))
 // Kernel-local lambdas must be inlined: an outlined call would take its
 // captures through memory and lose their wave-uniformity (the DMA needs
 // scalar operands).
 #define OOO_INLINE __attribute__((always_inline))
-
-// Workgroup barrier without the memory-model fence __syncthreads() adds.
-// The DMA is invisible to the compiler, so waits for it are explicit
-// (wait_vmcnt) before each barrier.  The "memory" clobber keeps the compiler
-// from moving LDS accesses across it.
-__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
 // LDS DMA of 16 bytes per lane from base + voff (base wave-uniform, voff
 // per lane); lane l's bytes land at LDS byte address lds + 16*l (lds
@@ -119,13 +111,6 @@ __device__ __forceinline__ float max3f(float a, float b, float c) {
   float r;
   asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
   return r;
-}
-
-// s_waitcnt vmcnt(n) (n <= 63), leaving the other counters alone.
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x0F70);
 }
 
 // LDS ring geometry for one head_dim.  A tile is 64 rows of K and 64 rows of
