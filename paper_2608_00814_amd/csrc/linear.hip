@@ -184,7 +184,18 @@ __device__ int tile_slots(long long C, int B, int KC, int seg, int t, int* slots
 // several batches) are all issued before the first add, so a sum costs one
 // round trip to memory rather than one per four slots; slots past the end of
 // the list re-read the last one and are not added.
-// fp16 partial values at element e of slot k: 4 (f32x4) or 1 (float)
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+// fp16 partial values at element e of slot k: 8 (f32x8), 4 (f32x4) or 1 (float)
+__device__ __forceinline__ void load_part(const Partials& p, int k, size_t stride, size_t e, f32x8& x, float& sc) {
+  const u32x4 h = *reinterpret_cast<const u32x4*>(p.v + k * stride + e);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const f32x2_t v = unpack_f16x2(h[i]);
+    x[2 * i] = v[0];
+    x[2 * i + 1] = v[1];
+  }
+  sc = p.sc[k * 4 + (int)(e % kRows) / 32];
+}
 __device__ __forceinline__ void load_part(const Partials& p, int k, size_t stride, size_t e, f32x4& x, float& sc) {
   const u32x2 h = *reinterpret_cast<const u32x2*>(p.v + k * stride + e);
   const f32x2_t lo = unpack_f16x2(h[0]), hi = unpack_f16x2(h[1]);
@@ -216,39 +227,40 @@ __device__ __forceinline__ T slot_sum_of(const Partials& part, const int* slots,
   return slot_batches<T, 16>(part, slots, ns, stride, e);
 }
 
-// Four blocks per output tile (per gate tile for kSwiGLU), 32 rows each;
-// thread item (n, 4 consecutive rows), so partial reads are 16 bytes and
-// contiguous across threads.
+// Four blocks per output tile (per gate tile for kSwiGLU): block q takes
+// tile rows 64 (q % 2) .. +63 of the nodes n = q / 2 (mod 2); thread item
+// (n, 8 consecutive rows), so every partial read is 16 bytes and eight
+// lanes read one node's whole 128-byte line.
 __global__ __launch_bounds__(256) void linear_reduce_kernel(Partials part, int N, int npad, int K,
                                                             int O, int B, int seg, int epi, void* __restrict__ out,
                                                             int inter) {
   __shared__ int slots[2][256];
   __shared__ int nslots[2];
-  const int t = blockIdx.x >> 2, quarter = blockIdx.x & 3;
+  const int t = blockIdx.x >> 2, half = blockIdx.x & 1, par = (blockIdx.x >> 1) & 1;
   const int KC = K / 64;
   const int tiles = (O + kRows - 1) / kRows;
   const long long C = (long long)tiles * KC;
   if (threadIdx.x < 2 && (threadIdx.x == 0 || epi == kSwiGLU))
     nslots[threadIdx.x] = tile_slots(C, B, KC, seg, threadIdx.x ? t + inter / kRows : t, slots[threadIdx.x]);
   __syncthreads();
-  const size_t stride = (size_t)npad * kRows;  // floats per slot
+  const size_t stride = (size_t)npad * kRows;  // elements per slot
   const int ns0 = nslots[0], ns1 = epi == kSwiGLU ? nslots[1] : 0;
-  for (int item = threadIdx.x; item < N * 8; item += 256) {
-    const int n = item >> 3, r = quarter * 32 + 4 * (item & 7);
+  for (int item = threadIdx.x; item < (N - par + 1) / 2 * 8; item += 256) {
+    const int n = 2 * (item >> 3) + par, r = half * 64 + 8 * (item & 7);
     const size_t e = (size_t)n * kRows + r;
     const int col = t * kRows + r;
-    const f32x4 sv = slot_sum_of<f32x4>(part, slots[0], ns0, stride, e);
+    const f32x8 sv = slot_sum_of<f32x8>(part, slots[0], ns0, stride, e);
     if (epi == kSwiGLU) {
-      const f32x4 uv = slot_sum_of<f32x4>(part, slots[1], ns1, stride, e);
+      const f32x8 uv = slot_sum_of<f32x8>(part, slots[1], ns1, stride, e);
       uint16_t* o = reinterpret_cast<uint16_t*>(out) + (size_t)n * inter + col;
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < 8; ++j)
         if (col + j < inter) o[j] = (uint16_t)(pack_bf16x2(sv[j] / (1.f + expf(-sv[j])) * uv[j], 0.f) & 0xFFFFu);
       continue;
     }
     const size_t o = (size_t)n * O + col;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < 8; ++j) {
       if (col + j >= O) break;
       if (epi == kStoreF32) reinterpret_cast<float*>(out)[o + j] = sv[j];
       else if (epi == kAddF32) reinterpret_cast<float*>(out)[o + j] += sv[j];
