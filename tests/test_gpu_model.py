@@ -97,6 +97,31 @@ def test_linear(N, K, O, packed):
     torch.cuda.synchronize()
 
 
+@pytest.mark.parametrize("scale", [3e4, 0.0])
+def test_linear_partials_beyond_fp16_range(scale):
+    """The stream-K partial sums pass through the workspace in fp16 with a
+    power-of-two factor per 32 rows: sums far beyond fp16's largest value
+    (65504) come back finite and within the fp32-output tolerance, and an
+    all-zero weight gives exact zeros."""
+    print(f"case linear partials scale={scale}", flush=True)
+    N, K, O = 16, 4096, 256
+    rs = np.random.default_rng(11)
+    x = _bits(rs, (N, K), max(scale, 1.0))
+    w = _bits(rs, (O, K), 1.0 if scale else 0.0)
+    ref = f64(x) @ f64(w).T
+    wp = ooo.linear_pack(_dev_bf16(w))
+    ws = torch.zeros(ooo.linear_workspace(N, K, O), dtype=torch.uint8, device=DEV)
+    y = torch.full((N, O), float("nan"), dtype=torch.float32, device=DEV)
+    ooo.linear(_dev_bf16(x), wp, y, ooo.EPI_STORE_F32, ws)
+    got = y.double().cpu().numpy()
+    assert np.isfinite(got).all()
+    if scale:
+        assert np.abs(ref).max() > 1e6  # every 64-column partial exceeds fp16's range
+        assert gh.row_rel_err(got, ref) <= F32_OUT_TOL
+    else:
+        assert (got == 0).all()
+
+
 @pytest.mark.parametrize("N,K,O", [(64, 4096, 4096), (37, 12288, 4096), (1, 256, 256), (5, 512, 1024),
                                    (64, 1024, 8192)])
 def test_linear_add_rmsnorm(N, K, O):
