@@ -118,14 +118,17 @@ __global__ __launch_bounds__(kStreamThreads) void linear_bf16_kernel(const uint1
     chunk_mfma<NB>(lds + stage * R::WS + wrow, lds + R::XREG + stage * R::XS, off, acc);
     if (q == total - 1 || kc == KC - 1) {
       // segment done: acc[nb][j] = partial of tile row wave*32 + 8(j/4) + 4u + j%4, node 32nb + c.
-      // Scale: the wave's largest magnitude a < 2^ex goes to [2^14, 2^15)
-      // (fp16 holds up to 65504); exact powers of two both ways.  Inf and
-      // NaN stay what they are.
+      // Scale: the wave's largest finite magnitude a < 2^ex goes to
+      // [2^14, 2^15) (fp16 holds up to 65504); exact powers of two both
+      // ways.  Inf and NaN stay what they are and do not set the scale.
       float amax = 0.f;
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-        for (int j = 0; j < 16; ++j) amax = __builtin_fmaxf(amax, __builtin_fabsf(acc[nb][j]));
+        for (int j = 0; j < 16; ++j) {
+          const float m = __builtin_fabsf(acc[nb][j]);
+          amax = __builtin_fmaxf(amax, m < INFINITY ? m : 0.f);
+        }
 #pragma unroll
       for (int o = 32; o > 0; o >>= 1) amax = __builtin_fmaxf(amax, shfl_xor_f(amax, o));
       const int ex = min(max(__builtin_amdgcn_frexp_expf(amax), -100), 100);

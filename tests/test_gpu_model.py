@@ -122,6 +122,28 @@ def test_linear_partials_beyond_fp16_range(scale):
         assert (got == 0).all()
 
 
+def test_linear_partials_keep_finite_rows_beside_an_infinite_one():
+    """An infinite input in one node's row makes that row's outputs
+    infinite or NaN; the other rows, whose partial sums share the fp16 scale
+    of the same 32 output columns, stay finite and accurate."""
+    print("case linear partials with an infinite row", flush=True)
+    N, K, O = 8, 1024, 128
+    rs = np.random.default_rng(12)
+    x = _bits(rs, (N, K))
+    w = _bits(rs, (O, K), 0.5)
+    x[3, 5] = np.uint16(0x7F80)  # +inf in bf16
+    wp = ooo.linear_pack(_dev_bf16(w))
+    ws = torch.zeros(ooo.linear_workspace(N, K, O), dtype=torch.uint8, device=DEV)
+    y = torch.full((N, O), float("nan"), dtype=torch.float32, device=DEV)
+    ooo.linear(_dev_bf16(x), wp, y, ooo.EPI_STORE_F32, ws)
+    got = y.double().cpu().numpy()
+    assert not np.isfinite(got[3]).any()
+    rows = [n for n in range(N) if n != 3]
+    ref = f64(x[rows]) @ f64(w).T
+    assert np.isfinite(got[rows]).all()
+    assert gh.row_rel_err(got[rows], ref) <= F32_OUT_TOL
+
+
 @pytest.mark.parametrize("N,K,O", [(64, 4096, 4096), (37, 12288, 4096), (1, 256, 256), (5, 512, 1024),
                                    (64, 1024, 8192)])
 def test_linear_add_rmsnorm(N, K, O):
