@@ -27,8 +27,9 @@
 //    of every tile (two waves per SIMD); head_dim 64: one wave per row group
 //    with a hand-pipelined tile loop.
 //  * Splits write fp16 partials (normalised O times a power of two, plus
-//    max, sum and scale in fp32) that a second kernel combines; with one
-//    split the kernel writes O directly.
+//    the split's log2 weight and the power's exponent, 8 bytes per row)
+//    that a second kernel combines, loading exactly the splits there are;
+//    with one split the kernel writes O directly.
 //  * Launch order is XCD-aware: consecutive work items (same KV head and
 //    row block, neighbouring splits) go to blocks that share blockIdx % 8,
 //    so one head's K/V stream stays in one XCD's L2.
@@ -59,7 +60,7 @@ struct AttnArgs {
   float scale_log2e;
   uint16_t* out;
   uint32_t* part_o;  // fp16 normalised partial outputs (fragment order)
-  float* part_ml;    // per partial row: max, sum, scale, unused
+  float* part_ml;    // per partial row: log2 of the split's weight, exponent of its scale
   int splits, row_blocks, Mpad, tiles_prefix, tiles_total;
   int tps;           // key tiles per split (split s takes tiles [s tps, (s + 1) tps))
   const int* P_dev;  // null, or the prefix length in device memory (P bounds it)
@@ -221,8 +222,8 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
 #pragma unroll
     for (int k = 0; k < R::GPL / 2; ++k) po[k * 64] = u32x4{0u, 0u, 0u, 0u};
     if (u == 0)
-      *reinterpret_cast<f32x4*>(a.part_ml + (((size_t)s * a.Hkv + g) * a.Mpad + row) * 4) =
-          f32x4{-INFINITY, 0.f, 1.f, 0.f};
+      *reinterpret_cast<f32x2_t*>(a.part_ml + (((size_t)s * a.Hkv + g) * a.Mpad + row) * 2) =
+          f32x2_t{-INFINITY, 0.f};
     return;
   }
 
@@ -406,13 +407,23 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
     if (tree || row0 + kTile > limit) {
       const uint64_t mw =
           !tree ? ~0ull : SPLIT ? mwords[(rg * 32 + c) * a.W + (t - tiles_prefix)] : mrow[t - tiles_prefix];
+      // A lane's values are two runs of 8 consecutive keys: each run's 8
+      // mask bits come from one shift.  (Testing a precomputed bit per key
+      // kept 48 registers live through the whole tile loop: 249 -> 200
+      // VGPRs for the key-split kernel, 16.40 -> 16.14 us per call at the
+      // Qwen3-8B shape.)
+      const int rem = limit - row0;  // keys of the tile inside the region
 #pragma unroll
       for (int hf = 0; hf < NH; ++hf)
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          const int off = 32 * (kh0 + hf) + 16 * (j / 8) + 8 * u + (j % 8);
-          const bool ok = (row0 + off < limit) && ((mw >> off) & 1ull);
-          if (!ok) acc[hf][j] = -INFINITY;
+        for (int g8 = 0; g8 < 2; ++g8) {
+          const int base = 32 * (kh0 + hf) + 16 * g8 + 8 * u;
+          const int inside = rem - base;
+          uint32_t bits = (uint32_t)(mw >> base) & 0xffu;
+          bits &= inside >= 8 ? 0xffu : inside <= 0 ? 0u : (1u << inside) - 1u;
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (!((bits >> e) & 1u)) acc[hf][8 * g8 + e] = -INFINITY;
         }
     }
   };
@@ -691,7 +702,8 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
   } else {
     // Split partial: the normalised output O/l (a convex combination of V
     // rows) in fp16, times 2^-e per row so that its largest magnitude lies
-    // in [0.5, 1), plus (max, sum, 2^e) in fp32.  Fragment order: for each
+    // in [0.5, 1), plus the split's weight m + log2(l) (its row max and sum
+    // in log2 units) and e, as two fp32 per row.  Fragment order: for each
     // (split, KV head, 32-row block) the lanes' O^T groups f = 4dt + q4 are
     // stored in pairs [f/2][lane] as 8 halves, so every store (and every
     // load of the combine) covers 1 KiB contiguously.
@@ -716,19 +728,20 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
       po[k * 64] = h;
     }
     if (u == 0)
-      *reinterpret_cast<f32x4*>(a.part_ml + (((size_t)s * a.Hkv + g) * a.Mpad + row) * 4) =
-          f32x4{m_run, l_tot, __builtin_amdgcn_ldexpf(1.f, ex), 0.f};
+      *reinterpret_cast<f32x2_t*>(a.part_ml + (((size_t)s * a.Hkv + g) * a.Mpad + row) * 2) =
+          f32x2_t{l_tot > 0.f ? m_run + __builtin_amdgcn_logf(l_tot) : -INFINITY, (float)ex};
   }
 }
 
 // Merge the splits of each query row:
-// O = sum_s 2^(m_s - m) l_s c_s P_s / sum_s 2^(m_s - m) l_s with m = max_s
-// m_s, where P_s is the stored fp16 partial and c_s its scale.  A split
-// that saw no allowed key has m_s = -inf and l_s = 0 and gets weight zero.
-// One wave per (KV head, 32-row block, pair of O^T groups): lane (c, u)
-// owns row c and the 8 columns 32(k/2) + 16(k%2) + 4u + {0..3, 8..11}.
-// Every load is issued before any arithmetic (one round trip to memory):
-// splits past the count re-read the last split and get weight zero.
+// O = sum_s 2^(w_s - w) 2^e_s P_s / sum_s 2^(w_s - w) with w = max_s w_s,
+// where w_s = m_s + log2(l_s) is the log2 weight of split s (its row max
+// and sum), P_s the stored fp16 partial and 2^e_s its scale.  A split that
+// saw no allowed key has w_s = -inf and gets weight zero.  One wave per
+// (KV head, 32-row block, pair of O^T groups): lane (c, u) owns row c and
+// the 8 columns 32(k/2) + 16(k%2) + 4u + {0..3, 8..11}.  Every load is
+// issued before any arithmetic (one round trip to memory): splits past the
+// count re-read the last split and get weight zero.
 // Waves per combine workgroup.  Two rather than four spreads the partial
 // reads over twice as many CUs: 15.95 -> 15.75 us per call (main kernel plus
 // combine) at the Qwen3-8B shape (64 nodes, 4k prefix, 13 splits).
@@ -753,26 +766,26 @@ __global__ __launch_bounds__(64 * kCombineWaves) void tree_attn_combine_kernel(A
   const size_t split_o = (size_t)a.Hkv * nblk * NP * 64;  // 16-byte units between consecutive splits
   const size_t split_ml = (size_t)a.Hkv * a.Mpad;         // rows between consecutive splits
   const u32x4* po = reinterpret_cast<const u32x4*>(a.part_o) + (((size_t)g * nblk + blk) * NP + k) * 64 + lane;
-  const f32x4* pml = reinterpret_cast<const f32x4*>(a.part_ml) + (size_t)g * a.Mpad + r;
-  f32x4 ml[SMAX];
+  const f32x2_t* pml = reinterpret_cast<const f32x2_t*>(a.part_ml) + (size_t)g * a.Mpad + r;
+  f32x2_t ml[SMAX];
   u32x4 o[SMAX];
 #pragma unroll
-  for (int s = 0; s < SMAX; ++s) {
+  for (int s = 0; s < SMAX; ++s) {  // splits past the count re-read the last one (weight zero below)
     const int sc = min(s, a.splits - 1);
     ml[s] = pml[sc * split_ml];
     o[s] = po[sc * split_o];
   }
   float m = -INFINITY;
 #pragma unroll
-  for (int s = 0; s < SMAX; ++s) m = __builtin_fmaxf(m, ml[s][0]);
+  for (int s = 0; s < SMAX; ++s) m = s < a.splits ? __builtin_fmaxf(m, ml[s][0]) : m;
   const float base = m == -INFINITY ? 0.f : m;
   float den = 0.f;
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int s = 0; s < SMAX; ++s) {
-    const float wgt = s < a.splits ? __builtin_amdgcn_exp2f(ml[s][0] - base) * ml[s][1] : 0.f;
+    const float wgt = s < a.splits ? __builtin_amdgcn_exp2f(ml[s][0] - base) : 0.f;
     den += wgt;
-    const float wv2 = wgt * ml[s][2];
+    const float wv2 = __builtin_amdgcn_ldexpf(wgt, (int)ml[s][1]);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const f32x2_t h = unpack_f16x2(o[s][e]);
@@ -873,6 +886,39 @@ __global__ __launch_bounds__(256) void tree_attn_f32_kernel(const float* q, cons
   }
 }
 
+// The combine kernel loads exactly the splits there are (up to 16; more in
+// groups of 4): each padding slot is one more load per lane, and the merge
+// is bound by its loads.
+template <int D, int S>
+void launch_combine_n(dim3 grid, hipStream_t st, const AttnArgs& a) {
+  tree_attn_combine_kernel<D, S><<<grid, 64 * kCombineWaves, 0, st>>>(a);
+}
+template <int D>
+void launch_combine(int splits, dim3 grid, hipStream_t st, const AttnArgs& a) {
+  switch (splits) {
+    case 2: return launch_combine_n<D, 2>(grid, st, a);
+    case 3: return launch_combine_n<D, 3>(grid, st, a);
+    case 4: return launch_combine_n<D, 4>(grid, st, a);
+    case 5: return launch_combine_n<D, 5>(grid, st, a);
+    case 6: return launch_combine_n<D, 6>(grid, st, a);
+    case 7: return launch_combine_n<D, 7>(grid, st, a);
+    case 8: return launch_combine_n<D, 8>(grid, st, a);
+    case 9: return launch_combine_n<D, 9>(grid, st, a);
+    case 10: return launch_combine_n<D, 10>(grid, st, a);
+    case 11: return launch_combine_n<D, 11>(grid, st, a);
+    case 12: return launch_combine_n<D, 12>(grid, st, a);
+    case 13: return launch_combine_n<D, 13>(grid, st, a);
+    case 14: return launch_combine_n<D, 14>(grid, st, a);
+    case 15: return launch_combine_n<D, 15>(grid, st, a);
+    case 16: return launch_combine_n<D, 16>(grid, st, a);
+    default:
+      if (splits <= 20) return launch_combine_n<D, 20>(grid, st, a);
+      if (splits <= 24) return launch_combine_n<D, 24>(grid, st, a);
+      if (splits <= 28) return launch_combine_n<D, 28>(grid, st, a);
+      return launch_combine_n<D, 32>(grid, st, a);
+  }
+}
+
 struct Plan {
   int waves, row_blocks, Mpad, tiles_prefix, tiles_total, splits, tps;
   size_t ws_bytes;
@@ -908,7 +954,7 @@ Plan make_plan(int N, int Hq, int Hkv, int D, int P, ooo_dtype dt, int force_spl
   p.tps = (p.tiles_total + splits - 1) / splits;
   p.splits = (p.tiles_total + p.tps - 1) / p.tps;
   if (p.splits > 1)
-    p.ws_bytes = (size_t)p.splits * Hkv * p.Mpad * (size_t)D * 2 + (size_t)p.splits * Hkv * p.Mpad * 16 + 256;
+    p.ws_bytes = (size_t)p.splits * Hkv * p.Mpad * (size_t)D * 2 + (size_t)p.splits * Hkv * p.Mpad * 8 + 256;
   return p;
 }
 
@@ -1012,15 +1058,8 @@ extern "C" int ooo_tree_attn_ex(const void* q, const void* k_cache, const void* 
     if (p.splits > 1) {
       const int waves = n_kv_heads * (p.Mpad / 32) * (head_dim / 16);
       const dim3 cgrid((waves + kCombineWaves - 1) / kCombineWaves);
-      if (head_dim == 128) {
-        if (p.splits <= 8) tree_attn_combine_kernel<128, 8><<<cgrid, 64 * kCombineWaves, 0, st>>>(a);
-        else if (p.splits <= 16) tree_attn_combine_kernel<128, 16><<<cgrid, 64 * kCombineWaves, 0, st>>>(a);
-        else tree_attn_combine_kernel<128, 32><<<cgrid, 64 * kCombineWaves, 0, st>>>(a);
-      } else {
-        if (p.splits <= 8) tree_attn_combine_kernel<64, 8><<<cgrid, 64 * kCombineWaves, 0, st>>>(a);
-        else if (p.splits <= 16) tree_attn_combine_kernel<64, 16><<<cgrid, 64 * kCombineWaves, 0, st>>>(a);
-        else tree_attn_combine_kernel<64, 32><<<cgrid, 64 * kCombineWaves, 0, st>>>(a);
-      }
+      if (head_dim == 128) launch_combine<128>(p.splits, cgrid, st, a);
+      else launch_combine<64>(p.splits, cgrid, st, a);
     }
   }
   const hipError_t e = hipGetLastError();
