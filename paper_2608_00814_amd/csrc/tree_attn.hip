@@ -486,7 +486,12 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
         qf[dk] = as_bf16x8(*reinterpret_cast<const u32x4*>(qs + (R::swz(rq, 2 * dk + u) << 4)));
     }
     if (ntiles > 2) issue(t_begin + 2, I2{});
-    bf16x8 pf_prev[2];  // wave B: probabilities of the previous tile
+    // Both waves of a pair run each tile as one matrix block (P V of the
+    // previous tile, then the scores of this one) and one vector block (the
+    // softmax): wave A (kh0 = 0) matrix block first, wave B (kh0 = 1)
+    // vector block first, so that on their SIMD the matrix cores work for
+    // one wave while the vector units work for the other.  A keeps the
+    // probabilities of the previous tile, B its scores.
     auto pv_tile = [&](auto stage_c, const bf16x8 (&pf)[2]) OOO_INLINE {
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
@@ -495,14 +500,22 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
         pv_mfma(vv, pf[ks]);
       }
     };
+    bf16x8 pf_hold[2];   // A: probabilities of the previous tile
+    f32x16 sc_hold[1];   // B: scores of the previous tile
+    auto softmax_tile = [&](int t, f32x16 (&sc)[1]) OOO_INLINE {
+      apply_mask(t, sc);
+      rescale(row_max(sc));
+      l_run += probs_half(sc[0], m_run == -INFINITY ? 0.f : m_run, pf_hold[0], pf_hold[1]);
+    };
     auto body = [&](auto role_c, int i, auto st_c) OOO_INLINE {
       constexpr bool B = decltype(role_c)::value;
       constexpr int ST = decltype(st_c)::value;
       if (i > 0) {
         wait_tiles<PER, 1>(min(1, ntiles - 1 - i));  // this wave's share of tile i landed
         wg_barrier();                                // ... and every other wave's
-        if (i + 2 < ntiles) issue(t_begin + i + 2, std::integral_constant<int, (ST + 2) % 4>{});
-        if constexpr (B) pv_tile(std::integral_constant<int, (ST + 3) % 4>{}, pf_prev);
+        if constexpr (B) softmax_tile(t_begin + i - 1, sc_hold);
+        __builtin_amdgcn_sched_barrier(0);
+        pv_tile(std::integral_constant<int, (ST + 3) % 4>{}, pf_hold);
       }
       f32x16 sc[1] = {f32x16{}};
       bf16x8 kf[1][4];
@@ -511,16 +524,15 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
         kread(st_c, b, kf);
         qk_mfma(b, kf, sc);
       }
-      apply_mask(t_begin + i, sc);
-      rescale(row_max(sc));
-      bf16x8 pf[2];
-      l_run += probs_half(sc[0], m_run == -INFINITY ? 0.f : m_run, pf[0], pf[1]);
-      if constexpr (!B) {
-        pv_tile(st_c, pf);
-      } else {
-        pf_prev[0] = pf[0];
-        pf_prev[1] = pf[1];
-        if (i == ntiles - 1) pv_tile(st_c, pf_prev);
+      // The DMA of tile i+2 (into the stage tile i-2 used, free since this
+      // tile's barrier) is issued once the matrix block is under way.
+      if (i > 0 && i + 2 < ntiles) issue(t_begin + i + 2, std::integral_constant<int, (ST + 2) % 4>{});
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (!B) softmax_tile(t_begin + i, sc);
+      else sc_hold[0] = sc[0];
+      if (i == ntiles - 1) {  // the last tile's P V
+        if constexpr (B) softmax_tile(t_begin + i, sc_hold);
+        pv_tile(st_c, pf_hold);
       }
     };
     auto run = [&](auto role_c) OOO_INLINE {
