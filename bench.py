@@ -170,6 +170,71 @@ def recorded_traffic(workload: str, entry: str):
     return int(rec["bytes_per_launch"])
 
 
+# Kernels whose counters make up each entry point's traffic, and the sources
+# whose digests decide whether a recorded profile still describes them.
+TRAFFIC_ENTRIES = {
+    "ooo_tree_attn": (("tree_attn_bf16_kernel", "tree_attn_combine_kernel"),
+                      ("paper_2608_00814_amd/csrc/tree_attn.hip", "paper_2608_00814_amd/csrc/device_common.h")),
+    "ooo_lmhead_argmax": (("lmhead_bf16_kernel", "lmhead_finalize_kernel"),
+                          ("paper_2608_00814_amd/csrc/lmhead.hip", "paper_2608_00814_amd/csrc/stream_core.h",
+                           "paper_2608_00814_amd/csrc/device_common.h")),
+}
+CALIBRATION_KERNEL = "CUDAFunctorOnSelf_add<float>"  # torch.add(src, 1.0, out=dst) of --calibrate-copy-mib
+
+
+def _short_kernel_name(name: str) -> str:
+    """'void ooo::(anonymous namespace)::k<1, 2>(args)' -> 'ooo::k<1, 2>'."""
+    name = name.replace("(anonymous namespace)::", "")
+    if name.startswith("void "):
+        name = name[5:]
+    depth = 0
+    for i, ch in enumerate(name):
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0:
+            return name[:i]
+    return name
+
+
+def counter_means(csv_path: str, counter: str):
+    """Mean value (KiB) of one rocprofv3 --pmc counter per dispatch, by
+    kernel (short name)."""
+    import csv
+    sums, counts = {}, {}
+    for row in csv.DictReader(open(csv_path)):
+        if row["Counter_Name"] != counter:
+            continue
+        k = _short_kernel_name(row["Kernel_Name"])
+        sums[k] = sums.get(k, 0.0) + float(row["Counter_Value"])
+        counts[k] = counts.get(k, 0) + 1
+    return {k: sums[k] / counts[k] for k in sums}
+
+
+def traffic_record(workload: str, fetch_csv: str, write_csv: str, calibrate_mib: int) -> dict:
+    """HBM bytes per launch of each entry point from one FETCH_SIZE and one
+    WRITE_SIZE profile of the same bench run.  Each counter is scaled by
+    what it reads for the calibration kernel, which reads and writes
+    calibrate_mib MiB; the sources' digests are stored with the numbers."""
+    fetch, write = counter_means(fetch_csv, "FETCH_SIZE"), counter_means(write_csv, "WRITE_SIZE")
+    cal = [k for k in fetch if CALIBRATION_KERNEL in k]
+    if len(cal) != 1 or cal[0] not in write:
+        raise ValueError("the profiles hold no single calibration copy (bench.py --calibrate-copy-mib)")
+    fs, ws = calibrate_mib * 1024.0 / fetch[cal[0]], calibrate_mib * 1024.0 / write[cal[0]]
+    rec = {"workload": workload, "fetch_scale": round(fs, 5), "write_scale": round(ws, 5)}
+    for entry, (parts, sources) in TRAFFIC_ENTRIES.items():
+        ks = sorted(k for k in fetch if any(p in k for p in parts))
+        if not ks:
+            continue
+        rec[entry] = {
+            "bytes_per_launch": int(round(sum((fetch[k] * fs + write.get(k, 0.0) * ws) * 1024 for k in ks))),
+            "kernels": {k: [fetch[k], write.get(k, 0.0)] for k in ks},
+            "sources": {f: _source_digest(f) for f in sources},
+        }
+    return rec
+
+
 def _blas_limit(cores: int):
     """Context manager pinning NumPy's BLAS pool to ``cores`` threads (a
     no-op without threadpoolctl)."""
@@ -807,9 +872,19 @@ def main():
     ap.add_argument("--no-graph", action="store_true", help="launch every kernel eagerly")
     ap.add_argument("--loop", action="store_true",
                     help="consecutive verify steps with compaction from the workload's prefix (wall clock)")
+    ap.add_argument("--record-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write profiles/hbm_traffic_<workload>.json from the counter_collection.csv files of a "
+                         "FETCH_SIZE and a WRITE_SIZE rocprofv3 run (no GPU needed)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="one plain copy of this many MiB after setup (byte-counter calibration)")
     args = ap.parse_args()
+    if args.record_traffic:
+        rec = traffic_record(args.workload, *args.record_traffic, calibrate_mib=args.calibrate_copy_mib or 1024)
+        path = os.path.join(ROOT, "profiles", f"hbm_traffic_{args.workload}.json")
+        with open(path, "w") as f:
+            json.dump(rec, f, indent=1)
+        print(json.dumps({k: v["bytes_per_launch"] for k, v in rec.items() if isinstance(v, dict)}))
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for {args.gpus}); the path runs on a single MI355X.",
               file=sys.stderr)

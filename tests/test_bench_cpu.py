@@ -97,3 +97,36 @@ def test_cpu_baseline_uses_every_core_of_the_affinity():
     with bench._blas_limit(cores):
         sizes = [i.get("num_threads") for i in threadpoolctl.threadpool_info() if i.get("user_api") == "blas"]
     assert all(n == cores for n in sizes)
+
+
+def _counter_csv(path, counter, rows):
+    head = ("Correlation_Id,Dispatch_Id,Agent_Id,Queue_Id,Process_Id,Thread_Id,Grid_Size,Kernel_Id,Kernel_Name,"
+            "Workgroup_Size,LDS_Block_Size,Scratch_Size,VGPR_Count,Accum_VGPR_Count,SGPR_Count,Counter_Name,"
+            "Counter_Value,Start_Timestamp,End_Timestamp")
+    lines = [head]
+    for i, (name, value) in enumerate(rows):
+        lines.append(f'{i},{i},"Agent 1",1,1,1,256,1,"{name}",256,0,0,4,0,16,"{counter}",{value},0,1')
+    path.write_text("\n".join(lines) + "\n")
+
+
+def test_traffic_record_from_counter_profiles(tmp_path):
+    """Per-launch bytes = sum over an entry point's kernels of mean FETCH
+    and WRITE KiB per dispatch, each scaled by what the counter reads for
+    the calibration copy of known size."""
+    attn = "void ooo::(anonymous namespace)::tree_attn_bf16_kernel<128, 4, true>(ooo::(anonymous namespace)::AttnArgs)"
+    comb = "void ooo::(anonymous namespace)::tree_attn_combine_kernel<128, 13>(ooo::(anonymous namespace)::AttnArgs)"
+    cal = ("void at::native::vectorized_elementwise_kernel<4, at::native::CUDAFunctorOnSelf_add<float>, "
+           "std::array<char*, 2ul> >(int, at::native::CUDAFunctorOnSelf_add<float>, std::array<char*, 2ul>)")
+    other = "void at::native::vectorized_elementwise_kernel<4, at::native::FillFunctor<int> >(int)"
+    f, w = tmp_path / "fetch.csv", tmp_path / "write.csv"
+    # the copy of 1 MiB: FETCH reads half its bytes (scale 2), WRITE all (scale 1)
+    _counter_csv(f, "FETCH_SIZE", [(cal, 512.0), (attn, 100.0), (attn, 300.0), (comb, 10.0), (other, 7.0)])
+    _counter_csv(w, "WRITE_SIZE", [(cal, 1024.0), (attn, 50.0), (attn, 50.0), (comb, 1.0), (other, 9.0)])
+    rec = bench.traffic_record("w", str(f), str(w), calibrate_mib=1)
+    assert rec["fetch_scale"] == 2.0 and rec["write_scale"] == 1.0
+    e = rec["ooo_tree_attn"]
+    assert set(e["kernels"]) == {"ooo::tree_attn_bf16_kernel<128, 4, true>", "ooo::tree_attn_combine_kernel<128, 13>"}
+    assert e["bytes_per_launch"] == ((200.0 * 2 + 50.0) + (10.0 * 2 + 1.0)) * 1024
+    assert "ooo_lmhead_argmax" not in rec  # no LM-head dispatch in these profiles
+    assert e["sources"]["paper_2608_00814_amd/csrc/tree_attn.hip"] == bench._source_digest(
+        "paper_2608_00814_amd/csrc/tree_attn.hip")
