@@ -261,6 +261,12 @@ LM_CASES = [
     (128, 512, 9999, "bf16"),
     (129, 64, 1000, "bf16"),
     (256, 256, 20000, "bf16"),
+    # more 128-row tiles than compute units with a partial last round: some
+    # blocks' last tile has only some of its 32-row groups (wide node tiles
+    # give a wave two groups, of which one, both or neither may be empty)
+    (128, 128, 40000, "bf16"),
+    (200, 64, 35000, "bf16"),
+    (256, 64, 70000, "bf16"),
     (25, 256, 1024, "f32"),
     (3, 100, 777, "f32"),
 ]
@@ -340,6 +346,29 @@ def test_lmhead_pack_layout(V, H):
     T, C = (V + 127) // 128, H // 64
     full = np.zeros((T * 128, H), np.uint16)
     full[:V] = w  # bf16 bit patterns
+    want = np.empty((T, C, 128, 8, 8), np.uint16)
+    for r in range(128):
+        for p in range(8):
+            q = p ^ (r % 8)
+            for kc in range(C):
+                want[:, kc, r, p, :] = full[r::128][:T, kc * 64 + 8 * q:kc * 64 + 8 * q + 8]
+    assert np.array_equal(got, want.reshape(-1))
+
+
+@pytest.mark.parametrize("O,K", [(384, 64), (300, 192)])
+def test_linear_pack_layout(O, K):
+    """The packed projection weight is a pure re-layout: tile t, chunk kc,
+    row r and physical 16-byte piece p hold columns kc*64 + 8*(p ^ r%8) .. +8
+    of row t*128 + r, and rows past out_dim are zero."""
+    print(f"case linear pack O={O} K={K}", flush=True)
+    rs = np.random.default_rng(O + K)
+    w = _bf16(rs.normal(size=(O, K)))
+    pw = ooo.linear_pack(gh.to_dev(w, "bf16", DEV))
+    torch.cuda.synchronize()
+    got = pw.data.cpu().numpy().view(np.uint16)
+    T, C = (O + 127) // 128, K // 64
+    full = np.zeros((T * 128, K), np.uint16)
+    full[:O] = w
     want = np.empty((T, C, 128, 8, 8), np.uint16)
     for r in range(128):
         for p in range(8):
