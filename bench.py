@@ -76,6 +76,98 @@ PAPER_CONTEXT = {
 PAPER_MAT_QWEN3_8B = 8.35  # tokens committed per verify call, Qwen3-8B on API-Bank (Table 2)
 
 
+# The other path workloads, timed kernel by kernel in the default run.
+SECONDARY_WORKLOADS = ("qwen3-0.6b", "qwen2.5-32b", "llama3.1-8b-decode")
+
+
+def kernel_record(cfg, N, attn_call_us, lm_us):
+    """Roofline figures of one tree-attention call and one LM head at a
+    workload's shapes (same byte and flop counts as the headline line)."""
+    a_bytes = attention_bytes(cfg, N)
+    a_flops = 4.0 * cfg.n_q_heads * N * cfg.prefix_len * cfg.head_dim
+    peak = MFMA_PEAK_TFLOPS if cfg.dtype == "bf16" else FP32_PEAK_TFLOPS
+    mfma_bound = a_flops / a_bytes > peak * 1e12 / (HBM_PEAK_GBS * 1e9)
+    a_gbs = a_bytes / (attn_call_us * 1e-6) / 1e9
+    a_tflops = a_flops / (attn_call_us * 1e-6) / 1e12
+    lm_gbs = lmhead_bytes(cfg, N) / (lm_us * 1e-6) / 1e9
+    return {"trie_nodes": N, "prefix_len": cfg.prefix_len,
+            "attention_us_per_call": round(attn_call_us, 3),
+            "attention_bound": "mfma" if mfma_bound else "hbm",
+            "attention_frac": round(a_tflops / peak if mfma_bound else a_gbs / HBM_PEAK_GBS, 4),
+            "attention_hbm_frac": round(a_gbs / HBM_PEAK_GBS, 4),
+            "attention_mfma_frac": round(a_tflops / peak, 4),
+            "lmhead_us": round(lm_us, 2), "lmhead_hbm_frac": round(lm_gbs / HBM_PEAK_GBS, 4)}
+
+
+def secondary_rates(name, dev, reps: int = 10):
+    """Tree attention and LM head at another workload's shapes: the
+    workload's own trie, K/V ~ N(0, 1) and LM-head weights ~ N(0, 0.02)
+    from a seeded device generator (the recipe's distributions without the
+    host-side generation of whole caches), enough distinct layer caches to
+    cycle past the 256 MiB last-level cache, one graph of those attention
+    calls, then the LM head; medians over reps."""
+    import torch
+
+    from paper_2608_00814_amd import workload as wl
+    from paper_2608_00814_amd.step import VerifyRunner
+
+    cfg = wl.CONFIGS[name]
+    tdt = torch.bfloat16
+    P = cfg.prefix_len
+    runner = VerifyRunner(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.hidden, cfg.vocab,
+                          cfg.max_nodes, cfg.max_depth, tdt, dev, max_prefix=P)
+    cand = wl.candidates_for(cfg, 0, 0)
+    runner.pack(cand.root_token, *cand.csr())
+    N = runner.n_nodes
+    runner.ensure_workspace(P)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(2608)
+    per_layer = 2 * cfg.n_kv_heads * cfg.cap * cfg.head_dim * 2
+    L = max(2, min(256, -(-(640 << 20) // per_layer)))
+    shp = (cfg.n_kv_heads, cfg.cap, cfg.head_dim)
+    k = torch.empty((L,) + shp, dtype=tdt, device=dev)
+    v = torch.empty((L,) + shp, dtype=tdt, device=dev)
+    for l in range(L):
+        k[l].copy_(torch.randn(shp, generator=gen, device=dev))
+        v[l].copy_(torch.randn(shp, generator=gen, device=dev))
+    q = torch.randn((N, cfg.n_q_heads, cfg.head_dim), generator=gen, device=dev).to(tdt)
+    w = (torch.randn((cfg.vocab, cfg.hidden), generator=gen, device=dev) * 0.02).to(tdt)
+    runner.set_weight(w)
+    del w
+    hidden = torch.randn((N, cfg.hidden), generator=gen, device=dev).to(tdt)
+    torch.cuda.synchronize()
+    stream = torch.cuda.Stream()  # default priority
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    attn_us, lm_us = [], []
+    with torch.cuda.stream(stream):
+        runner.upload_tree()
+
+        def attend():
+            for l in range(L):
+                runner.attention(l % cfg.n_layers, q, k[l], v[l], P)
+
+        attend()
+        runner.lm_head(hidden)
+        stream.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=stream):
+            attend()
+        for _ in range(reps):
+            ev[0].record(stream)
+            graph.replay()
+            ev[1].record(stream)
+            runner.lm_head(hidden)
+            ev[2].record(stream)
+            stream.synchronize()
+            attn_us.append(1e3 * ev[0].elapsed_time(ev[1]) / L)
+            lm_us.append(1e3 * ev[1].elapsed_time(ev[2]))
+    rec = kernel_record(cfg, N, float(np.median(attn_us)), float(np.median(lm_us)))
+    rec["layer_caches_cycled"] = L
+    del graph, k, v, q, hidden, runner
+    torch.cuda.empty_cache()
+    return rec
+
+
 def step_time_stats(step_s):
     """Median and 10th/90th percentiles of per-step wall times (ms)."""
     a = np.asarray(step_s, dtype=np.float64) * 1e3
@@ -870,6 +962,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="launch every kernel eagerly")
+    ap.add_argument("--no-others", action="store_true",
+                    help="skip the kernel timings at the other workloads' shapes (default run only)")
     ap.add_argument("--loop", action="store_true",
                     help="consecutive verify steps with compaction from the workload's prefix (wall clock)")
     ap.add_argument("--record-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -1129,9 +1223,11 @@ def main():
                                "attention_us_per_layer": round(f_attn_us / cfg.n_layers, 3),
                                "lmhead_us": round(f_lm_us, 2), "path_hbm_gbs": round(f_path_gbs, 1),
                                "path_hbm_frac": round(f_path_gbs / HBM_PEAK_GBS, 4)}
+    del k_cache, v_cache
+    torch.cuda.empty_cache()
+    if args.workload == "qwen3-8b" and not args.no_others and not args.no_graph:
+        out["other_workloads"] = {name: secondary_rates(name, dev) for name in SECONDARY_WORKLOADS}
     if not args.no_cpu_baseline:
-        del k_cache, v_cache
-        torch.cuda.empty_cache()
         out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 

@@ -13,6 +13,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 sys.path.insert(0, ROOT)
 
 import bench  # noqa: E402
+import math  # noqa: E402
 from paper_2608_00814_amd import workload as wl  # noqa: E402
 
 
@@ -130,3 +131,26 @@ def test_traffic_record_from_counter_profiles(tmp_path):
     assert "ooo_lmhead_argmax" not in rec  # no LM-head dispatch in these profiles
     assert e["sources"]["paper_2608_00814_amd/csrc/tree_attn.hip"] == bench._source_digest(
         "paper_2608_00814_amd/csrc/tree_attn.hip")
+
+
+def test_kernel_record_at_the_other_workloads():
+    """The other workloads' kernel figures use the headline's byte and flop
+    counts: an HBM-bound shape is graded against 8 TB/s, an MFMA-bound one
+    against the bf16 matrix peak."""
+    c4 = wl.CONFIGS["qwen2.5-32b"]
+    N = 128
+    kv = 2 * c4.n_kv_heads * (c4.prefix_len + N) * c4.head_dim * 2
+    qo = 2 * N * c4.n_q_heads * c4.head_dim * 2
+    flops = 4.0 * c4.n_q_heads * N * c4.prefix_len * c4.head_dim
+    rec = bench.kernel_record(c4, N, attn_call_us=40.0, lm_us=300.0)
+    assert rec["attention_bound"] == "mfma"  # 4 Hq N P D / bytes is above the 312 flop/B ridge
+    assert math.isclose(rec["attention_mfma_frac"], flops / 40e-6 / 1e12 / 2500.0, rel_tol=1e-3)
+    assert rec["attention_frac"] == rec["attention_mfma_frac"]
+    assert math.isclose(rec["attention_hbm_frac"], (kv + qo) / 40e-6 / 1e9 / 8000.0, rel_tol=1e-3)
+    lm = c4.vocab * c4.hidden * 2 + N * c4.hidden * 2 + N * 8
+    assert math.isclose(rec["lmhead_hbm_frac"], lm / 300e-6 / 1e9 / 8000.0, rel_tol=1e-3)
+    c2 = wl.CONFIGS["qwen3-0.6b"]
+    rec2 = bench.kernel_record(c2, 32, attn_call_us=10.0, lm_us=60.0)
+    assert rec2["attention_bound"] == "hbm"
+    assert rec2["attention_frac"] == rec2["attention_hbm_frac"]
+    assert set(bench.SECONDARY_WORKLOADS) <= set(wl.CONFIGS)
