@@ -270,16 +270,21 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
 #pragma unroll
       for (int i = 0; i < PM; ++i) dma16_nt(vb, dvoff[i], vl + i * NW * 1024);
     } else {
+      uint32_t vo[PM];
 #pragma unroll
       for (int i = 0; i < PM; ++i) {
         const int r = (i * NW + wave) * R::RPI + lane / R::CH;
         const int rc = min(r, limit - 1 - row0);
-        const uint32_t vo = rc * R::ROWB + R::swz(r, lane % R::CH) * 16;
-        dma16_nt(kb, vo, kl + i * NW * 1024);
-        dma16_nt(vb, vo, vl + i * NW * 1024);
+        vo[i] = rc * R::ROWB + R::swz(r, lane % R::CH) * 16;
       }
+#pragma unroll
+      for (int i = 0; i < PM; ++i) dma16_nt(kb, vo[i], kl + i * NW * 1024);
+#pragma unroll
+      for (int i = 0; i < PM; ++i) dma16_nt(vb, vo[i], vl + i * NW * 1024);
     }
   };
+  // Every tile issues its PM K instructions before its PM V instructions,
+  // so waiting until PM are pending leaves only the tile's V in flight.
 
   // The mask words go through LDS so that no global load is pending inside
   // the tile loop, where a wait for it would also wait for the tile DMA.
@@ -475,7 +480,11 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
     // 1 is requested only now: with every block asking for tiles 0 and 1 at
     // once, each block's tile 0 lands later (15.57 -> 15.41 us per call at
     // the Qwen3-8B shape, graphs of 36 calls).
-    wait_vmcnt<0>();
+    // Only K of tile 0 (and Q, the mask words) must have landed: V of tile
+    // 0 is first read after barrier 1, whose wait covers it (with a single
+    // tile it is read before any other wait, so then wait for it too).
+    if (ntiles > 1) wait_vmcnt<PM>();
+    else wait_vmcnt<0>();
     __syncthreads();
     if (ntiles > 1) issue(t_begin + 1, I1{});
     {
