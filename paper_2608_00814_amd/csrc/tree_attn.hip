@@ -959,12 +959,17 @@ Plan make_plan(int N, int Hq, int Hkv, int D, int P, ooo_dtype dt, int force_spl
   p.tiles_total = p.tiles_prefix + (N + kTile - 1) / kTile;
   // Split count: as many workgroups as fit on the CUs at once, balancing the
   // tiles of the busiest split against the partials every split adds (an
-  // empirical cost of about 1.3 us per 64-key tile and 0.5 us per split).
+  // empirical cost of about 1.3 us per 64-key tile and 0.5 us per split of
+  // 128-row blocks, half that for 64-row blocks, whose partials are half
+  // the size: at 32 nodes, 2 query heads per KV head and a 1k prefix, 9
+  // splits take 9.96 us per call and the 6 of the 128-row cost 10.8 us).
+  // Units of 0.05 us.
   const int base = Hkv * p.row_blocks;
   const int max_splits = device_cus() / base > 1 ? device_cus() / base : 1;
+  const int split_cost = p.waves == 2 ? 5 : 10;
   int splits = 1, best = INT32_MAX;
   for (int sc = 1; sc <= max_splits && sc <= p.tiles_total; ++sc) {
-    const int cost = 13 * ((p.tiles_total + sc - 1) / sc) + 5 * sc;
+    const int cost = 26 * ((p.tiles_total + sc - 1) / sc) + split_cost * sc;
     if (cost < best) best = cost, splits = sc;
   }
   if (force_splits > 0) splits = force_splits;
