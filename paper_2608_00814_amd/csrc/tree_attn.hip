@@ -763,10 +763,13 @@ __global__ __launch_bounds__(64 * RG * (SPLIT ? 2 : 1)) void tree_attn_bf16_kern
 // the 8 columns 32(k/2) + 16(k%2) + 4u + {0..3, 8..11}.  Every load is
 // issued before any arithmetic (one round trip to memory): splits past the
 // count re-read the last split and get weight zero.
-// Waves per combine workgroup.  Two rather than four spreads the partial
-// reads over twice as many CUs: 15.95 -> 15.75 us per call (main kernel plus
-// combine) at the Qwen3-8B shape (64 nodes, 4k prefix, 13 splits).
-constexpr int kCombineWaves = 2;
+// Waves per combine workgroup: one, so that the partial reads spread over
+// as many CUs as possible.  Main kernel plus combine per call, each pair
+// timed in one process: at the Qwen3-8B shape (64 nodes, 4k prefix, 13
+// splits) four waves 15.95 against two 15.75 us, two 15.28 against one
+// 15.25 us; at the Qwen3-0.6B shape (32 nodes, 1k prefix, 9 splits) two
+// 9.96 against one 9.74 us.
+constexpr int kCombineWaves = 1;
 
 template <int D, int SMAX>
 __global__ __launch_bounds__(64 * kCombineWaves) void tree_attn_combine_kernel(AttnArgs a) {
