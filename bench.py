@@ -99,6 +99,18 @@ def kernel_record(cfg, N, attn_call_us, lm_us):
             "lmhead_us": round(lm_us, 2), "lmhead_hbm_frac": round(lm_gbs / HBM_PEAK_GBS, 4)}
 
 
+def tp8_shard_config():
+    """One GPU's share of the Qwen3-8B shape under 8-way tensor parallelism
+    over KV heads and vocabulary rows: 1 KV head with its 4 query heads, and
+    1/8 of the LM-head rows (the trie is the full step's)."""
+    import dataclasses
+
+    from paper_2608_00814_amd import workload as wl
+    c3 = wl.CONFIGS["qwen3-8b"]
+    return dataclasses.replace(c3, n_q_heads=c3.n_q_heads // 8, n_kv_heads=c3.n_kv_heads // 8,
+                               vocab=c3.vocab // 8)
+
+
 def secondary_rates(name, dev, reps: int = 10):
     """Tree attention and LM head at another workload's shapes: the
     workload's own trie, K/V ~ N(0, 1) and LM-head weights ~ N(0, 0.02)
@@ -111,7 +123,7 @@ def secondary_rates(name, dev, reps: int = 10):
     from paper_2608_00814_amd import workload as wl
     from paper_2608_00814_amd.step import VerifyRunner
 
-    cfg = wl.CONFIGS[name]
+    cfg = wl.CONFIGS[name] if isinstance(name, str) else name
     tdt = torch.bfloat16
     P = cfg.prefix_len
     runner = VerifyRunner(cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.hidden, cfg.vocab,
@@ -1227,6 +1239,11 @@ def main():
     torch.cuda.empty_cache()
     if args.workload == "qwen3-8b" and not args.no_others and not args.no_graph:
         out["other_workloads"] = {name: secondary_rates(name, dev) for name in SECONDARY_WORKLOADS}
+        shard = secondary_rates(tp8_shard_config(), dev)
+        shard["note"] = ("one GPU's share of the Qwen3-8B step under 8-way tensor parallelism (1 KV head, "
+                         "4 query heads, 1/8 of the vocabulary rows); the all-gather of N x 8 B per step "
+                         "is not included")
+        out["tp8_shard"] = shard
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -154,3 +154,13 @@ def test_kernel_record_at_the_other_workloads():
     assert rec2["attention_bound"] == "hbm"
     assert rec2["attention_frac"] == rec2["attention_hbm_frac"]
     assert set(bench.SECONDARY_WORKLOADS) <= set(wl.CONFIGS)
+
+
+def test_tp8_shard_shape():
+    """One GPU's share under 8-way tensor parallelism keeps the query heads
+    per KV head and the trie, with an eighth of the heads and vocabulary."""
+    c3 = wl.CONFIGS["qwen3-8b"]
+    s = bench.tp8_shard_config()
+    assert (s.n_kv_heads, s.n_q_heads, s.vocab) == (1, 4, c3.vocab // 8)
+    assert s.group == c3.group and s.max_nodes == c3.max_nodes and s.prefix_len == c3.prefix_len
+    assert bench.attention_bytes(s, 64) * 8 == bench.attention_bytes(c3, 64)
