@@ -202,6 +202,32 @@ def test_attention_split_counts_agree(splits):
     assert gh.row_rel_err(a, ref) <= gh.ATTN_TOL
 
 
+# (P, N, G, Hkv, D, splits, variant): a split whose first key tile crosses
+# the end of the prefix (the last prefix tile is partly masked) and which
+# goes on to further tiles, in the key-split kernel (variant 0) and the
+# one-wave kernel (variant 1 at head_dim 128, and head_dim 64)
+BOUNDARY_SPLITS = [
+    (150, 64, 4, 2, 128, 2, 0),   # tiles [0,1] [2,3]: split 1 starts at tile 2 (rows 128..191, prefix 150)
+    (150, 64, 4, 2, 128, 2, 1),
+    (190, 130, 4, 1, 128, 3, 0),  # tiles [0,1] [2,3] [4,5]: 3 mask words, the last tree tile partial too
+    (190, 130, 2, 2, 64, 3, 0),
+]
+
+
+@pytest.mark.parametrize("case", BOUNDARY_SPLITS, ids=[f"P{c[0]}-N{c[1]}-G{c[2]}-Hkv{c[3]}-D{c[4]}-S{c[5]}-v{c[6]}"
+                                                       for c in BOUNDARY_SPLITS])
+def test_attention_split_starting_at_a_boundary_tile(case):
+    P, N, G, Hkv, D, splits, variant = case
+    print(f"case attention boundary split {case}", flush=True)
+    rs, q, k, v, cap = _attn_inputs(P, N, G, Hkv, D, "bf16", seed=P * N + splits)
+    t = _trie("random", N, rs)
+    W = (N + 63) // 64
+    mask = ov.ancestor_masks(t["parent"], W)
+    got = _run_attn(q, k, v, P, N, mask, G * Hkv, Hkv, D, "bf16", force_splits=splits, variant=variant)
+    ref = ov.tree_attention(wl.to_f64(q, "bf16"), wl.to_f64(k, "bf16"), wl.to_f64(v, "bf16"), P, t["parent"], Hkv)
+    assert gh.row_rel_err(got, ref) <= gh.ATTN_TOL
+
+
 def test_attention_workspace_reuse_across_shapes():
     """One workspace serves calls of different shapes, head sizes and split
     counts in a row: nothing a call reads from it is left over from another
