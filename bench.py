@@ -228,6 +228,20 @@ def copy_bandwidth_gbs(dev, mib: int = 1024, reps: int = 10) -> float:
     return 2.0 * (mib << 20) / sec / 1e9
 
 
+def calibration_copy(mib: int, dev) -> None:
+    """One plain elementwise copy that reads and writes ``mib`` MiB each (the
+    byte counters' calibration kernel); nothing when mib is 0."""
+    if mib <= 0:
+        return
+    import torch
+    src = torch.ones(mib << 18, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    torch.add(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    del src, dst
+
+
 def _source_digest(path: str) -> str:
     """sha256 prefix of a source file with comments and whitespace removed."""
     text = open(os.path.join(ROOT, path)).read()
@@ -283,6 +297,14 @@ TRAFFIC_ENTRIES = {
                           ("paper_2608_00814_amd/csrc/lmhead.hip", "paper_2608_00814_amd/csrc/stream_core.h",
                            "paper_2608_00814_amd/csrc/device_common.h")),
 }
+# The projection kernels of one fused decoder layer (ModelRunner.forward):
+# four streaming products (qkv, o, gate+up, down), then the qkv epilogue
+# (norms, rotation, cache writes), two residual-add + RMSNorm epilogues and
+# the SwiGLU reduce.  Count per layer, and the sources they are built from.
+MODEL_PROJECTION_KERNELS = {"linear_bf16_kernel": 4, "linear_add_rmsnorm_kernel": 2,
+                            "linear_qk_norm_rope_kernel": 1, "linear_reduce_kernel": 1}
+MODEL_PROJECTION_SOURCES = ("paper_2608_00814_amd/csrc/linear.hip", "paper_2608_00814_amd/csrc/stream_core.h",
+                            "paper_2608_00814_amd/csrc/rope.h", "paper_2608_00814_amd/csrc/device_common.h")
 CALIBRATION_KERNEL = "CUDAFunctorOnSelf_add<float>"  # torch.add(src, 1.0, out=dst) of --calibrate-copy-mib
 
 
@@ -320,13 +342,30 @@ def traffic_record(workload: str, fetch_csv: str, write_csv: str, calibrate_mib:
     """HBM bytes per launch of each entry point from one FETCH_SIZE and one
     WRITE_SIZE profile of the same bench run.  Each counter is scaled by
     what it reads for the calibration kernel, which reads and writes
-    calibrate_mib MiB; the sources' digests are stored with the numbers."""
+    calibrate_mib MiB; the sources' digests are stored with the numbers.
+    For a full-model workload the one entry is "projections": the bytes of
+    every projection kernel of one verify step (all layers)."""
     fetch, write = counter_means(fetch_csv, "FETCH_SIZE"), counter_means(write_csv, "WRITE_SIZE")
     cal = [k for k in fetch if CALIBRATION_KERNEL in k]
     if len(cal) != 1 or cal[0] not in write:
         raise ValueError("the profiles hold no single calibration copy (bench.py --calibrate-copy-mib)")
     fs, ws = calibrate_mib * 1024.0 / fetch[cal[0]], calibrate_mib * 1024.0 / write[cal[0]]
     rec = {"workload": workload, "fetch_scale": round(fs, 5), "write_scale": round(ws, 5)}
+    from paper_2608_00814_amd import model_workload as mw
+    if workload in mw.MODEL_CONFIGS:
+        n_layers = mw.MODEL_CONFIGS[workload].n_layers
+        kernels = {}
+        for part, per_layer in MODEL_PROJECTION_KERNELS.items():
+            ks = [k for k in fetch if part in k]
+            if len(ks) != 1:
+                raise ValueError(f"expected one instantiation of {part} in the profile, found {ks}")
+            kernels[ks[0]] = [fetch[ks[0]], write.get(ks[0], 0.0), per_layer * n_layers]
+        rec["projections"] = {
+            "bytes_per_launch": int(round(sum((f * fs + w * ws) * 1024 * n for f, w, n in kernels.values()))),
+            "kernels": kernels,
+            "sources": {f: _source_digest(f) for f in MODEL_PROJECTION_SOURCES},
+        }
+        return rec
     for entry, (parts, sources) in TRAFFIC_ENTRIES.items():
         ks = sorted(k for k in fetch if any(p in k for p in parts))
         if not ks:
@@ -545,6 +584,7 @@ def bench_model(args):
             runner.device_step(k_cache, v_cache, P)
         stream.synchronize()
     setup_s = time.time() - t_setup
+    calibration_copy(args.calibrate_copy_mib, dev)
 
     # per-phase breakdown on eager steps (outside the timed steps)
     with torch.cuda.stream(stream):
@@ -1059,14 +1099,7 @@ def main():
     torch.cuda.synchronize()
     setup_s = time.time() - t_setup
 
-    if args.calibrate_copy_mib > 0:
-        n = args.calibrate_copy_mib << 18  # float32 elements
-        src = torch.ones(n, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        torch.add(src, 1.0, out=dst)  # reads and writes calibrate_copy_mib MiB each
-        torch.cuda.synchronize()
-        del src, dst
+    calibration_copy(args.calibrate_copy_mib, dev)
 
     stream = torch.cuda.Stream()  # default priority
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]

@@ -133,6 +133,38 @@ def test_traffic_record_from_counter_profiles(tmp_path):
         "paper_2608_00814_amd/csrc/tree_attn.hip")
 
 
+def test_traffic_record_of_the_model_projections(tmp_path):
+    """Full-model workload: one "projections" entry, the bytes of every
+    projection kernel of one verify step (mean per dispatch times the
+    dispatches of a step: per-layer count times the layers)."""
+    from paper_2608_00814_amd import model_workload as mw
+    cal = ("void at::native::vectorized_elementwise_kernel<4, at::native::CUDAFunctorOnSelf_add<float>, "
+           "std::array<char*, 2ul> >(int, at::native::CUDAFunctorOnSelf_add<float>, std::array<char*, 2ul>)")
+    names = {"linear_bf16_kernel": "void ooo::(anonymous namespace)::linear_bf16_kernel<2, true>(int)",
+             "linear_add_rmsnorm_kernel": "void ooo::(anonymous namespace)::linear_add_rmsnorm_kernel(int)",
+             "linear_qk_norm_rope_kernel": "void ooo::(anonymous namespace)::linear_qk_norm_rope_kernel<128>(int)",
+             "linear_reduce_kernel": "void ooo::(anonymous namespace)::linear_reduce_kernel(int)"}
+    kib = {"linear_bf16_kernel": (40.0, 4.0), "linear_add_rmsnorm_kernel": (3.0, 2.0),
+           "linear_qk_norm_rope_kernel": (2.0, 1.0), "linear_reduce_kernel": (5.0, 1.0)}
+    attn = "void ooo::(anonymous namespace)::tree_attn_bf16_kernel<128, 4, true>(int)"
+    f, w = tmp_path / "fetch.csv", tmp_path / "write.csv"
+    # two dispatches of the streaming kernel with different sizes: the mean counts
+    frows = [(cal, 512.0), (attn, 99.0)] + [(names[k], v[0]) for k, v in kib.items()]
+    frows.append((names["linear_bf16_kernel"], 60.0))
+    wrows = [(cal, 1024.0), (attn, 99.0)] + [(names[k], v[1]) for k, v in kib.items()]
+    wrows.append((names["linear_bf16_kernel"], 6.0))
+    _counter_csv(f, "FETCH_SIZE", frows)
+    _counter_csv(w, "WRITE_SIZE", wrows)
+    rec = bench.traffic_record("small-model", str(f), str(w), calibrate_mib=1)
+    assert set(rec) == {"workload", "fetch_scale", "write_scale", "projections"}
+    L = mw.MODEL_CONFIGS["small-model"].n_layers
+    e = rec["projections"]
+    want = L * 1024 * (4 * (50.0 * 2 + 5.0) + 2 * (3.0 * 2 + 2.0) + (2.0 * 2 + 1.0) + (5.0 * 2 + 1.0))
+    assert e["bytes_per_launch"] == int(round(want))
+    assert e["kernels"]["ooo::linear_bf16_kernel<2, true>"] == [50.0, 5.0, 4 * L]
+    assert set(e["sources"]) == set(bench.MODEL_PROJECTION_SOURCES)
+
+
 def test_kernel_record_at_the_other_workloads():
     """The other workloads' kernel figures use the headline's byte and flop
     counts: an HBM-bound shape is graded against 8 TB/s, an MFMA-bound one
