@@ -192,8 +192,9 @@ __global__ __launch_bounds__(kStreamThreads) void lmhead_bf16_kernel(const uint1
 
 // Packed weight layout: for tile t (128 rows) and chunk kc (64 columns), the
 // 16 KiB block at ((t * chunks + kc) * 128 + r) * 64 elements holds row
-// t*128 + r; its physical 16-byte piece p holds columns kc*64 + 8*(p ^ r%8)
-// .. +8, the swizzle the kernel's LDS reads expect.  Rows >= V are zero.
+// t*128 + r; its physical 16-byte piece p holds columns
+// kc*64 + 8*(p ^ (r/2)%8) .. +8, the swizzle the kernel's LDS reads expect.
+// Rows >= V are zero.
 __global__ __launch_bounds__(256) void lmhead_pack_kernel(const uint16_t* __restrict__ W, int V, int H,
                                                           uint16_t* __restrict__ out, long long pieces) {
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
@@ -206,7 +207,7 @@ __global__ __launch_bounds__(256) void lmhead_pack_kernel(const uint16_t* __rest
   const long long t = tk / chunks;
   const long long row = t * kLmRows + r;
   u32x4 v = {0, 0, 0, 0};
-  if (row < V) v = ld16(W + row * H + kc * 64 + ((p ^ (r % 8)) * 8));
+  if (row < V) v = ld16(W + row * H + kc * 64 + ((p ^ piece_swz(r)) * 8));
   st16(out + i * 8, v);
 }
 

@@ -6,9 +6,13 @@
 //    four 32-row slots of 4 KiB.  In the packed layout (ooo_lmhead_pack)
 //    chunk (t, kc) is one contiguous 16 KiB block, already swizzled; in the
 //    row layout (nn.Linear) a slot is gathered row by row.
-//  * In LDS the 16-byte piece p of row r sits at piece p ^ (r % 8), so the
-//    DMA rows (8 per instruction) and the MFMA fragment reads (16 lanes, 16
-//    rows, one piece) both hit distinct banks.
+//  * In LDS the 16-byte piece p of row r sits at piece p ^ ((r / 2) % 8).
+//    A 128-byte row covers half of gfx950's 64 LDS banks, so even and odd
+//    rows fall in opposite halves, and a 16-byte read serves 16 lanes (16
+//    rows, one piece) at a time: with the XOR by (r / 2) % 8 the eight rows
+//    in each half read eight different pieces, all 64 banks once.  (An XOR
+//    by r % 8 gave rows r and r + 8 the same banks: a 2-way conflict on
+//    every fragment read.)
 //  * Seven waves per block: four compute waves own 32 W rows each; two
 //    loader waves DMA the W slots (two each) and a third the X chunk into a
 //    ring of NS stages, NS - 1 chunks requested ahead of the one consumed.
@@ -23,6 +27,9 @@ namespace ooo {
 
 constexpr int kStreamRows = 128;  // W rows per tile (4 compute waves x 32)
 constexpr int kStreamThreads = 448;  // 4 compute waves + 2 W loaders + 1 X loader
+
+// physical piece of logical piece p in LDS row r (and in the packed layout)
+__device__ __forceinline__ int piece_swz(int r) { return (r >> 1) & 7; }
 
 template <int NB>
 struct StreamRing {
@@ -67,7 +74,7 @@ __device__ __forceinline__ void dma_w_slot_rows(const uint16_t* W, long long ld,
 #pragma unroll
   for (int jj = 0; jj < 4; ++jj) {
     const int r = 8 * jj + lane / 8;
-    const int pc = (lane % 8) ^ (r % 8);
+    const int pc = (lane % 8) ^ piece_swz(r);
     const int row = min(row0 + r, rows - 1);
     __builtin_amdgcn_global_load_lds(OOO_GLB(W + (size_t)row * ld + kc * 64 + pc * 8), OOO_LDS(dst + jj * 1024),
                                      16, 0, kStreamOnce);
@@ -80,7 +87,7 @@ __device__ __forceinline__ void dma_x_chunk(const uint16_t* X, int N, long long 
 #pragma unroll
   for (int j = 0; j < StreamRing<NB>::XDMA; ++j) {
     const int r = 8 * j + lane / 8;
-    const int pc = (lane % 8) ^ (r % 8);
+    const int pc = (lane % 8) ^ piece_swz(r);
     const int row = min(r, N - 1);
     __builtin_amdgcn_global_load_lds(OOO_GLB(X + (size_t)row * ld + kc * 64 + pc * 8), OOO_LDS(dst + j * 1024), 16, 0,
                                      0);
@@ -107,7 +114,7 @@ __device__ __forceinline__ void loader_stream(int total, Issue&& issue) {
 __device__ __forceinline__ void frag_offsets(int lane, uint32_t (&off)[4]) {
   const int c = lane & 31, u = lane >> 5;
 #pragma unroll
-  for (int s4 = 0; s4 < 4; ++s4) off[s4] = c * 128 + (((2 * s4 + u) ^ (c % 8)) << 4);
+  for (int s4 = 0; s4 < 4; ++s4) off[s4] = c * 128 + (((2 * s4 + u) ^ piece_swz(c)) << 4);
 }
 
 // One chunk of a compute wave: acc[nb] += (its 32 W rows at Ws) x (node

@@ -361,7 +361,7 @@ def test_lmhead_exact_ties_go_to_lowest_index(packed):
 @pytest.mark.parametrize("V,H", [(1000, 64), (128, 128), (300, 192)])
 def test_lmhead_pack_layout(V, H):
     """The packed weight is a pure re-layout: tile t, chunk kc, row r and
-    physical 16-byte piece p hold columns kc*64 + 8*(p ^ r%8) .. +8 of row
+    physical 16-byte piece p hold columns kc*64 + 8*(p ^ (r//2)%8) .. +8 of row
     t*128 + r, and rows past the vocabulary are zero."""
     print(f"case lmhead pack V={V} H={H}", flush=True)
     rs = np.random.default_rng(V + H)
@@ -375,7 +375,7 @@ def test_lmhead_pack_layout(V, H):
     want = np.empty((T, C, 128, 8, 8), np.uint16)
     for r in range(128):
         for p in range(8):
-            q = p ^ (r % 8)
+            q = p ^ ((r // 2) % 8)
             for kc in range(C):
                 want[:, kc, r, p, :] = full[r::128][:T, kc * 64 + 8 * q:kc * 64 + 8 * q + 8]
     assert np.array_equal(got, want.reshape(-1))
@@ -384,7 +384,7 @@ def test_lmhead_pack_layout(V, H):
 @pytest.mark.parametrize("O,K", [(384, 64), (300, 192)])
 def test_linear_pack_layout(O, K):
     """The packed projection weight is a pure re-layout: tile t, chunk kc,
-    row r and physical 16-byte piece p hold columns kc*64 + 8*(p ^ r%8) .. +8
+    row r and physical 16-byte piece p hold columns kc*64 + 8*(p ^ (r//2)%8) .. +8
     of row t*128 + r, and rows past out_dim are zero."""
     print(f"case linear pack O={O} K={K}", flush=True)
     rs = np.random.default_rng(O + K)
@@ -398,7 +398,7 @@ def test_linear_pack_layout(O, K):
     want = np.empty((T, C, 128, 8, 8), np.uint16)
     for r in range(128):
         for p in range(8):
-            q = p ^ (r % 8)
+            q = p ^ ((r // 2) % 8)
             for kc in range(C):
                 want[:, kc, r, p, :] = full[r::128][:T, kc * 64 + 8 * q:kc * 64 + 8 * q + 8]
     assert np.array_equal(got, want.reshape(-1))
