@@ -106,9 +106,9 @@ def tp8_shard_config():
     import dataclasses
 
     from paper_2608_00814_amd import workload as wl
-    c3 = wl.CONFIGS["qwen3-8b"]
-    return dataclasses.replace(c3, n_q_heads=c3.n_q_heads // 8, n_kv_heads=c3.n_kv_heads // 8,
-                               vocab=c3.vocab // 8)
+    q8b = wl.CONFIGS["qwen3-8b"]
+    return dataclasses.replace(q8b, n_q_heads=q8b.n_q_heads // 8, n_kv_heads=q8b.n_kv_heads // 8,
+                               vocab=q8b.vocab // 8)
 
 
 def secondary_rates(name, dev, reps: int = 10):

@@ -169,20 +169,20 @@ def test_kernel_record_at_the_other_workloads():
     """The other workloads' kernel figures use the headline's byte and flop
     counts: an HBM-bound shape is graded against 8 TB/s, an MFMA-bound one
     against the bf16 matrix peak."""
-    c4 = wl.CONFIGS["qwen2.5-32b"]
+    q32b = wl.CONFIGS["qwen2.5-32b"]
     N = 128
-    kv = 2 * c4.n_kv_heads * (c4.prefix_len + N) * c4.head_dim * 2
-    qo = 2 * N * c4.n_q_heads * c4.head_dim * 2
-    flops = 4.0 * c4.n_q_heads * N * c4.prefix_len * c4.head_dim
-    rec = bench.kernel_record(c4, N, attn_call_us=40.0, lm_us=300.0)
+    kv = 2 * q32b.n_kv_heads * (q32b.prefix_len + N) * q32b.head_dim * 2
+    qo = 2 * N * q32b.n_q_heads * q32b.head_dim * 2
+    flops = 4.0 * q32b.n_q_heads * N * q32b.prefix_len * q32b.head_dim
+    rec = bench.kernel_record(q32b, N, attn_call_us=40.0, lm_us=300.0)
     assert rec["attention_bound"] == "mfma"  # 4 Hq N P D / bytes is above the 312 flop/B ridge
     assert math.isclose(rec["attention_mfma_frac"], flops / 40e-6 / 1e12 / 2500.0, rel_tol=1e-3)
     assert rec["attention_frac"] == rec["attention_mfma_frac"]
     assert math.isclose(rec["attention_hbm_frac"], (kv + qo) / 40e-6 / 1e9 / 8000.0, rel_tol=1e-3)
-    lm = c4.vocab * c4.hidden * 2 + N * c4.hidden * 2 + N * 8
+    lm = q32b.vocab * q32b.hidden * 2 + N * q32b.hidden * 2 + N * 8
     assert math.isclose(rec["lmhead_hbm_frac"], lm / 300e-6 / 1e9 / 8000.0, rel_tol=1e-3)
-    c2 = wl.CONFIGS["qwen3-0.6b"]
-    rec2 = bench.kernel_record(c2, 32, attn_call_us=10.0, lm_us=60.0)
+    q06b = wl.CONFIGS["qwen3-0.6b"]
+    rec2 = bench.kernel_record(q06b, 32, attn_call_us=10.0, lm_us=60.0)
     assert rec2["attention_bound"] == "hbm"
     assert rec2["attention_frac"] == rec2["attention_hbm_frac"]
     assert set(bench.SECONDARY_WORKLOADS) <= set(wl.CONFIGS)
@@ -191,8 +191,8 @@ def test_kernel_record_at_the_other_workloads():
 def test_tp8_shard_shape():
     """One GPU's share under 8-way tensor parallelism keeps the query heads
     per KV head and the trie, with an eighth of the heads and vocabulary."""
-    c3 = wl.CONFIGS["qwen3-8b"]
+    q8b = wl.CONFIGS["qwen3-8b"]
     s = bench.tp8_shard_config()
-    assert (s.n_kv_heads, s.n_q_heads, s.vocab) == (1, 4, c3.vocab // 8)
-    assert s.group == c3.group and s.max_nodes == c3.max_nodes and s.prefix_len == c3.prefix_len
-    assert bench.attention_bytes(s, 64) * 8 == bench.attention_bytes(c3, 64)
+    assert (s.n_kv_heads, s.n_q_heads, s.vocab) == (1, 4, q8b.vocab // 8)
+    assert s.group == q8b.group and s.max_nodes == q8b.max_nodes and s.prefix_len == q8b.prefix_len
+    assert bench.attention_bytes(s, 64) * 8 == bench.attention_bytes(q8b, 64)
